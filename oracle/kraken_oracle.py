@@ -1,0 +1,187 @@
+"""Plain fp64 CPU oracle for the Kraken prefill forward pass.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import this module:
+it is used by ``tests/``, by ``__graft_entry__.smoke()`` and by the
+``cpu_baseline`` leg of ``bench.py``, and by nothing else.  It shares no code
+with the HIP path (no kernels, headers, layouts or helpers); the two meet only
+in the seeded input arrays that the tests hand to both.
+
+What it computes (Prabhakar, Zhang and Wentzlaff, "Kraken: Inherently Parallel
+Transformers For Efficient Multi-Device Inference", arXiv 2408.07802):
+
+* Algorithm 1 ("Kraken Sub-Layer: Forward Pass"): for one sub-layer with
+  input ``x`` and the combined activations ``y`` of the previous layer,
+      h   = x + MHA(LN1(x))
+      out = h + FFN(LN2(h + y)).
+  The first layer uses ``y = x`` (the AllReduce is replaced by the identity).
+* Section 3.1 (layer construction): ``y`` is the element-wise sum of the N
+  sub-layer outputs of the previous layer, added before the FFN LayerNorm;
+  all first-layer sub-layers share one input; after the last layer the N
+  outputs are concatenated and multiplied by ``W_concat`` (Nd x d).
+* Section 2.1 (background): MHA is ``softmax(Q K^T / sqrt(h)) V`` per head with
+  ``h`` the head dimension, heads combined by the output projection; the FFN is
+  two linears with a GELU in between; LayerNorms sit before MHA and FFN
+  (pre-LN).
+
+Readings where the paper is silent (each is restated in the design doc):
+LayerNorm uses the biased variance and eps = 1e-5; GELU is the exact erf form;
+all four linears carry a bias, ``W_concat`` does not; the causal mask applies
+within each packed sequence only; ``y`` includes the sub-layer's own input
+(an AllReduce sums every participant).
+
+Every function works in float64 on whatever values it is given; callers pass
+the exact dtype-rounded inputs and weights of the run being checked.
+
+Weight layout taken by this module (a convention, not mathematics): every
+matrix multiplies as ``u @ W`` (row-major ``[in, out]``); ``Wqkv`` has
+columns ``[Q | K | V]`` and head ``h`` owns columns ``h*hd:(h+1)*hd`` of each.
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Iterable, Mapping, Sequence
+
+import numpy as np
+from scipy.special import erf as _erf
+
+LN_EPS = 1e-5
+
+# Names of the per-(layer, sub-layer) parameters, as the oracle reads them.
+PARAM_NAMES = ("ln1_g", "ln1_b", "Wqkv", "bqkv", "Wo", "bo",
+               "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+def layer_norm(v: np.ndarray, gamma, beta, eps: float = LN_EPS) -> np.ndarray:
+    """Pre-LN LayerNorm over the last axis (Section 2.1; Algorithm 1).
+
+    ``gamma * (v - mean) / sqrt(var + eps) + beta`` with the biased variance.
+    """
+    v = _f64(v)
+    mu = v.mean(axis=-1, keepdims=True)
+    var = ((v - mu) ** 2).mean(axis=-1, keepdims=True)
+    return _f64(gamma) * (v - mu) / np.sqrt(var + eps) + _f64(beta)
+
+
+def gelu(z: np.ndarray) -> np.ndarray:
+    """Exact GELU, ``z * Phi(z) = z/2 * (1 + erf(z / sqrt 2))`` (Section 2.1)."""
+    z = _f64(z)
+    return 0.5 * z * (1.0 + _erf(z / math.sqrt(2.0)))
+
+
+def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int) -> np.ndarray:
+    """Scaled dot-product attention with a causal mask, per head and per sequence.
+
+    Section 2.1: each head computes ``softmax(Q K^T / sqrt(hd)) V``.  ``Q, K, V``
+    are ``[T, d]`` with head ``h`` in columns ``h*hd:(h+1)*hd``; tokens of packed
+    sequence ``b`` are rows ``cu[b]:cu[b+1]`` and attend to themselves and to
+    earlier tokens of the same sequence only.  Returns the heads concatenated,
+    ``[T, d]``.
+    """
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    T, d = Q.shape
+    hd = d // n_heads
+    out = np.zeros((T, d), dtype=np.float64)
+    for b in range(len(cu_seqlens) - 1):
+        s0, s1 = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+        S = s1 - s0
+        future = np.triu(np.ones((S, S), dtype=bool), k=1)   # key index > query index
+        for h in range(n_heads):
+            cols = slice(h * hd, (h + 1) * hd)
+            scores = Q[s0:s1, cols] @ K[s0:s1, cols].T / math.sqrt(hd)
+            scores[future] = -np.inf
+            scores -= scores.max(axis=1, keepdims=True)
+            p = np.exp(scores)
+            p /= p.sum(axis=1, keepdims=True)
+            out[s0:s1, cols] = p @ V[s0:s1, cols]
+    return out
+
+
+def multi_head_attention(u, p: Mapping, cu_seqlens, n_heads: int) -> np.ndarray:
+    """MHA block: QKV projection, per-head causal attention, output projection."""
+    u = _f64(u)
+    d = u.shape[1]
+    qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
+    Q, K, V = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    return causal_attention(Q, K, V, cu_seqlens, n_heads) @ _f64(p["Wo"]) + _f64(p["bo"])
+
+
+def feed_forward(u, p: Mapping) -> np.ndarray:
+    """FFN block: two linears with the exact GELU between them (Section 2.1)."""
+    u = _f64(u)
+    return gelu(u @ _f64(p["W1"]) + _f64(p["b1"])) @ _f64(p["W2"]) + _f64(p["b2"])
+
+
+def sub_layer_forward(x, y, p: Mapping, cu_seqlens, n_heads: int,
+                      eps: float = LN_EPS) -> np.ndarray:
+    """One Kraken sub-layer (Algorithm 1) given its input ``x`` and combined ``y``.
+
+    ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.
+    """
+    x = _f64(x)
+    h = x + multi_head_attention(layer_norm(x, p["ln1_g"], p["ln1_b"], eps),
+                                 p, cu_seqlens, n_heads)
+    return h + feed_forward(layer_norm(h + _f64(y), p["ln2_g"], p["ln2_b"], eps), p)
+
+
+def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mapping]],
+                   W_concat, n_heads: int, eps: float = LN_EPS):
+    """Forward pass of a stack of Kraken layers followed by ``W_concat``.
+
+    ``X`` is the shared first-layer input ``[T, d]`` (Section 3.1: one set of
+    embeddings feeds every first-layer sub-layer).  ``layers`` yields, per layer,
+    a sequence of N parameter mappings (one per sub-layer); it may be a lazy
+    iterable so that large stacks are materialised one layer at a time.
+
+    Per layer j: ``y = X`` if j is the first layer (Algorithm 1's comment), else
+    ``y = sum_k x_k`` over the N outputs of the previous layer (Section 3.1,
+    element-wise addition); then every sub-layer runs Algorithm 1.
+
+    Returns ``(out, sub_out)``: ``sub_out[i]`` is sub-layer i's output after the
+    last layer (``[N, T, d]``) and ``out = [Y_1 | ... | Y_N] @ W_concat``
+    (``[T, d]``; Section 3.1, final combine).
+    """
+    X = _f64(X)
+    xs = None
+    for j, layer in enumerate(layers):
+        n_sub = len(layer)
+        if j == 0:
+            xs = [X] * n_sub
+            y = X
+        else:
+            if len(xs) != n_sub:
+                raise ValueError("every layer must have the same number of sub-layers")
+            y = np.sum(xs, axis=0)
+        xs = [sub_layer_forward(xs[i], y, layer[i], cu_seqlens, n_heads, eps)
+              for i in range(n_sub)]
+    if xs is None:
+        raise ValueError("at least one layer is required")
+    Y = np.concatenate(xs, axis=1)          # [T, N*d]
+    out = Y @ _f64(W_concat)
+    return out, np.stack(xs)
+
+
+def kraken_param_count(n_sub: int, n_layers: int, d: int, d_ff: int,
+                       vocab: int = 0, biases: bool = True, layer_norms: bool = True,
+                       w_concat: bool = True, positions: int = 0) -> int:
+    """Number of parameters of a Kraken model.
+
+    Per sub-layer: QKV (3d^2) + output projection (d^2) + FFN (2 d d_ff), plus
+    optional biases (3d + d + d_ff + d) and two LayerNorms (4d) -- Section 3.2's
+    closed form counts only the matrices.  ``W_concat`` adds N d^2 (Section 3.1),
+    token and position embeddings add ``(vocab + positions) * d``.
+    """
+    per_sub = 4 * d * d + 2 * d * d_ff
+    if biases:
+        per_sub += 3 * d + d + d_ff + d
+    if layer_norms:
+        per_sub += 4 * d
+    total = n_layers * n_sub * per_sub
+    if w_concat:
+        total += n_sub * d * d
+    total += (vocab + positions) * d
+    return total

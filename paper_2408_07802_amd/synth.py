@@ -1,0 +1,157 @@
+"""Seeded synthetic workloads for the Kraken prefill.
+
+This module only draws numbers: it holds none of the method's arithmetic, and it
+is the one thing the HIP path and the fp64 oracle share (the same input arrays,
+not code).  Every tensor is keyed by ``(seed, tensor id, layer, sub-layer)`` so any
+single tensor can be regenerated on its own, on the host or on a device.  Values
+are drawn in fp32 and rounded once (round-to-nearest-even) to the workload's
+storage dtype; both sides then use exactly those values.
+
+Workload shapes and distributions follow the paper's TTFT setting (random
+weights, batch 1, causal prefill; Section 4.3) at the sizes listed in
+``WORKLOADS``: hidden input ~ N(0, 1), weights ~ N(0, 0.02), LayerNorm
+gamma = 1 / beta = 0 and zero biases, with the 1/sqrt(2L)-scaled residual
+projections where a workload asks for them (Section 3.1 describes that kind of
+scaled initialisation).  ``affine="random"`` draws biases ~ N(0, 0.02),
+gamma ~ 1 + N(0, 0.1) and beta ~ N(0, 0.02) instead, so that those code paths
+are exercised by the parity tests.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import math
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+__all__ = ["Workload", "WORKLOADS", "workload", "seq_lens", "cu_seqlens",
+           "gen_hidden", "gen_sub_layer", "gen_layer", "gen_w_concat", "torch_dtype"]
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    n_sub: int                 # N parallel sub-layers per layer
+    n_layers: int              # L
+    d_model: int               # d, width of one sub-layer
+    n_heads: int               # heads per sub-layer
+    d_ff: int                  # MLP width
+    dtype: str                 # "f32" or "bf16" storage dtype
+    seq_lens: Optional[Sequence[int]] = None   # fixed lengths (None: drawn, see ragged)
+    ragged: Optional[tuple] = None             # (count, lo, hi): lengths ~ U{lo..hi}
+    w_std: float = 0.02
+    out_proj_std: Optional[float] = None       # std of Wo and W2 (None: w_std)
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_heads
+
+
+WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
+    Workload("kraken-n2-l2-d128-h4-s64-f32", 2, 2, 128, 4, 512, "f32", seq_lens=(64,)),
+    Workload("kraken-n4-l12-d768-h12-s2048-bf16", 4, 12, 768, 12, 3072, "bf16",
+             seq_lens=(2048,)),
+    Workload("kraken-n4-l24-d1024-h16-s4096-bf16", 4, 24, 1024, 16, 4096, "bf16",
+             seq_lens=(4096,), out_proj_std=0.02 / math.sqrt(2 * 24)),
+    Workload("kraken-n8-l24-d2048-h16-s8192-bf16", 8, 24, 2048, 16, 8192, "bf16",
+             seq_lens=(8192,)),
+    Workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16", 4, 36, 1280, 20, 5120, "bf16",
+             ragged=(8, 512, 4096)),
+]}
+
+# The workload the throughput benchmark runs: N=8 sub-layers of width 2048, 24 layers,
+# one causal sequence of 8192 tokens.
+BENCH_WORKLOAD = "kraken-n8-l24-d2048-h16-s8192-bf16"
+
+_TENSOR_IDS = {"hidden": 1, "ln1_g": 2, "ln1_b": 3, "Wqkv": 4, "bqkv": 5, "Wo": 6, "bo": 7,
+               "ln2_g": 8, "ln2_b": 9, "W1": 10, "b1": 11, "W2": 12, "b2": 13,
+               "W_concat": 14, "lens": 15}
+
+
+def workload(name: str) -> Workload:
+    return WORKLOADS[name]
+
+
+def torch_dtype(w: Workload) -> torch.dtype:
+    return {"f32": torch.float32, "bf16": torch.bfloat16}[w.dtype]
+
+
+def _key(*parts: int) -> int:
+    h = hashlib.sha256(",".join(str(int(p)) for p in parts).encode()).digest()
+    return int.from_bytes(h[:8], "little") & ((1 << 63) - 1)
+
+
+def _normal(shape, key: int, std: float, mean: float, device, dtype) -> torch.Tensor:
+    g = torch.Generator(device=device)
+    g.manual_seed(key)
+    t = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    if std != 1.0:
+        t.mul_(std)
+    if mean != 0.0:
+        t.add_(mean)
+    return t.to(dtype)
+
+
+def seq_lens(w: Workload, seed: int = 0) -> List[int]:
+    if w.seq_lens is not None:
+        return list(w.seq_lens)
+    count, lo, hi = w.ragged
+    rng = np.random.default_rng([seed, _TENSOR_IDS["lens"]])
+    return [int(v) for v in rng.integers(lo, hi + 1, size=count)]
+
+
+def cu_seqlens(lens: Sequence[int]) -> List[int]:
+    cu = [0]
+    for s in lens:
+        cu.append(cu[-1] + int(s))
+    return cu
+
+
+def gen_hidden(w: Workload, n_tokens: int, seed: int = 0, device="cpu") -> torch.Tensor:
+    """Shared first-layer input ``[T, d]`` ~ N(0, 1)."""
+    return _normal((n_tokens, w.d_model), _key(seed, _TENSOR_IDS["hidden"]), 1.0, 0.0,
+                   device, torch_dtype(w))
+
+
+def gen_sub_layer(w: Workload, layer: int, sub: int, seed: int = 0, device="cpu",
+                  affine: str = "plain") -> Dict[str, torch.Tensor]:
+    """Parameters of sub-layer ``sub`` of layer ``layer`` (x @ W layout, [in, out])."""
+    d, f = w.d_model, w.d_ff
+    dt = torch_dtype(w)
+    ostd = w.out_proj_std if w.out_proj_std is not None else w.w_std
+
+    def mat(name, shape, std):
+        return _normal(shape, _key(seed, _TENSOR_IDS[name], layer, sub), std, 0.0, device, dt)
+
+    def vec(name, n, kind):
+        if affine == "plain":
+            fill = 1.0 if kind == "gamma" else 0.0
+            return torch.full((n,), fill, dtype=dt, device=device)
+        std, mean = {"gamma": (0.1, 1.0), "beta": (0.02, 0.0), "bias": (0.02, 0.0)}[kind]
+        return _normal((n,), _key(seed, _TENSOR_IDS[name], layer, sub, 1), std, mean,
+                       device, dt)
+
+    if affine not in ("plain", "random"):
+        raise ValueError(f"unknown affine variant {affine!r}")
+    return {
+        "ln1_g": vec("ln1_g", d, "gamma"), "ln1_b": vec("ln1_b", d, "beta"),
+        "Wqkv": mat("Wqkv", (d, 3 * d), w.w_std), "bqkv": vec("bqkv", 3 * d, "bias"),
+        "Wo": mat("Wo", (d, d), ostd), "bo": vec("bo", d, "bias"),
+        "ln2_g": vec("ln2_g", d, "gamma"), "ln2_b": vec("ln2_b", d, "beta"),
+        "W1": mat("W1", (d, f), w.w_std), "b1": vec("b1", f, "bias"),
+        "W2": mat("W2", (f, d), ostd), "b2": vec("b2", d, "bias"),
+    }
+
+
+def gen_layer(w: Workload, layer: int, seed: int = 0, device="cpu",
+              affine: str = "plain") -> List[Dict[str, torch.Tensor]]:
+    return [gen_sub_layer(w, layer, i, seed, device, affine) for i in range(w.n_sub)]
+
+
+def gen_w_concat(w: Workload, seed: int = 0, device="cpu") -> torch.Tensor:
+    """``W_concat`` ``[N*d, d]`` ~ N(0, 0.02)."""
+    return _normal((w.n_sub * w.d_model, w.d_model), _key(seed, _TENSOR_IDS["W_concat"]),
+                   w.w_std, 0.0, device, torch_dtype(w))
