@@ -1,0 +1,260 @@
+/*
+ * kraken.h -- C ABI of the MI355X (gfx950) Kraken prefill library.
+ *
+ * Method: Prabhakar, Zhang and Wentzlaff, "Kraken: Inherently Parallel
+ * Transformers For Efficient Multi-Device Inference" (arXiv 2408.07802).
+ *
+ * A Kraken model is a stack of L layers; every layer holds N independent
+ * pre-LN Transformer sub-layers of width d (Section 3.1).  Sub-layer i of
+ * layer j runs Algorithm 1 ("Kraken Sub-Layer: Forward Pass"):
+ *
+ *     h_i      = x_i + MHA_i(LN1_i(x_i))
+ *     x_i(j+1) = h_i + FFN_i(LN2_i(h_i + y(j)))
+ *
+ * with y(1) = X (the first layer replaces the AllReduce by the identity) and
+ * y(j) = sum_k x_k(j) for j >= 2 (the element-wise sum of the previous
+ * layer's N outputs, Section 3.1).  All first-layer sub-layers read the same
+ * input X.  After layer L the outputs are combined by one linear map,
+ * out = [Y_1 | ... | Y_N] W_concat with W_concat of shape (N d) x d
+ * (Section 3.1).  MHA is causal scaled dot-product attention per head,
+ * softmax(Q K^T / sqrt(hd)) V with hd = d / heads, heads combined by the
+ * output projection; FFN is Linear -> exact GELU -> Linear (Section 2.1).
+ * LayerNorm uses the biased variance.  On one GPU the N sub-layers of a layer
+ * run as batched work and the paper's cross-device AllReduce becomes an
+ * on-device N-way sum fused into the FFN LayerNorm.
+ *
+ * Conventions shared by every call
+ *   - All calls return a kraken_status; no C++ exception crosses this ABI.
+ *     On failure kraken_last_error() returns a thread-local detail string.
+ *   - Validation happens before anything is enqueued: a call that fails
+ *     validation has enqueued no work.  Launch failures return
+ *     KRAKEN_ERR_HIP; faults inside kernels surface at the caller's next
+ *     synchronisation of the stream.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device work is asynchronous and ordered on that stream.
+ *   - Device pointers must be device memory of the device that was current
+ *     when the model was created; that device must be current at every call.
+ */
+#ifndef KRAKEN_H_
+#define KRAKEN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KRAKEN_OK = 0,
+  KRAKEN_ERR_INVALID_ARG = 1,  /* a null pointer, a bad size, a bad cu_seqlens */
+  KRAKEN_ERR_UNSUPPORTED = 2,  /* a valid configuration this build does not implement */
+  KRAKEN_ERR_OOM = 3,          /* device allocation failed; nothing is leaked */
+  KRAKEN_ERR_STATE = 4,        /* e.g. kraken_prefill before kraken_load_weights */
+  KRAKEN_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed */
+} kraken_status;
+
+typedef enum {
+  KRAKEN_DTYPE_F32 = 0,
+  KRAKEN_DTYPE_BF16 = 1,
+  KRAKEN_DTYPE_F16 = 2
+} kraken_dtype;
+
+/* MFMA operand type of every projection and of attention (accumulation is
+ * always fp32, and so are the residual stream, LayerNorm statistics and the
+ * softmax).  KRAKEN_COMPUTE_STORAGE uses the storage dtype.  Weights are
+ * converted once at load; a weight that does not fit the operand type (an
+ * fp16 overflow) makes kraken_load_weights fail with UNSUPPORTED. */
+typedef enum {
+  KRAKEN_COMPUTE_STORAGE = 0,
+  KRAKEN_COMPUTE_F32 = 1,
+  KRAKEN_COMPUTE_BF16 = 2,
+  KRAKEN_COMPUTE_F16 = 3
+} kraken_compute;
+
+/*
+ * Model shape (Section 3.1; heads are per sub-layer as in the paper's engine
+ * table, Section 4.3).
+ *   n_sub      N >= 1, parallel sub-layers per layer
+ *   n_layers   L >= 1
+ *   d_model    d, width of one sub-layer; multiple of 64
+ *   n_heads    heads per sub-layer; d / n_heads must be 32, 64 or 128
+ *   d_ff       MLP width; 0 means 4 d (Section 2.1); multiple of 64
+ *   max_tokens largest packed token count T a prefill may use (>= 1)
+ *   dtype      a kraken_dtype: element type of the weight blob and of hidden_in
+ *   compute    a kraken_compute: MFMA operand type (0 = same as dtype)
+ *   ln_eps     LayerNorm epsilon; 0 means 1e-5
+ */
+typedef struct {
+  int32_t n_sub;
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t d_ff;
+  int32_t max_tokens;
+  int32_t dtype;
+  int32_t compute;
+  float ln_eps;
+} kraken_config;
+
+typedef struct kraken_model kraken_model;
+
+/* Largest number of packed sequences one kraken_prefill call accepts. */
+#define KRAKEN_MAX_SEQS 256
+
+/* Row stride of the transposed-V operand of kraken_op_attention for T tokens. */
+#define KRAKEN_VT_LD(T) ((((T) + 63) / 64) * 64)
+
+/*
+ * Creates a model on the current device and allocates all device memory it
+ * will use (weights and the activation workspace for max_tokens tokens).
+ * The model owns that memory until kraken_destroy.  *out is set to NULL on
+ * failure.  Errors: INVALID_ARG (null pointers, non-positive sizes),
+ * UNSUPPORTED (d or d_ff not a multiple of 64, head size not 32/64/128,
+ * unknown dtype), OOM.
+ */
+kraken_status kraken_create(const kraken_config* cfg, kraken_model** out);
+
+/*
+ * Number of elements of the weight blob for cfg (0 for an invalid cfg):
+ *   L * N * (4 d^2 + 2 d F + 9 d + F) + N d^2.
+ */
+size_t kraken_weight_blob_elems(const kraken_config* cfg);
+
+/*
+ * Loads the weights.  The blob holds elements of the model's dtype in this
+ * logical order: for j in 0..L-1, for i in 0..N-1 (sub-layer i of layer j):
+ *   ln1_g[d] ln1_b[d] Wqkv[d][3d] bqkv[3d] Wo[d][d] bo[d]
+ *   ln2_g[d] ln2_b[d] W1[d][F] b1[F] W2[F][d] b2[d]
+ * and then W_concat[N d][d].  Matrices are row-major and multiply as x W
+ * ([in][out]); Wqkv's columns are [Q | K | V] and head h owns columns
+ * h*hd .. h*hd+hd-1 of each; W_concat's row block i multiplies Y_i.
+ * blob_is_device selects whether `blob` is device or host memory.  The call
+ * copies and repacks the blob into the model's own layout; the caller keeps
+ * ownership and may free or reuse the blob once the stream has synchronised.
+ * Errors: INVALID_ARG (null, nbytes != elems * dtype size), UNSUPPORTED (a
+ * weight outside the range of the compute type; the call then synchronises
+ * the stream to read the check), HIP.  A host blob is uploaded through a
+ * staging buffer and the call returns after the upload.
+ */
+kraken_status kraken_load_weights(kraken_model* m, const void* blob, size_t nbytes,
+                                  int blob_is_device, void* stream);
+
+/*
+ * Prefill forward pass of the whole stack (Algorithm 1 over L layers, then
+ * W_concat) for a packed batch of num_seqs causal sequences.
+ *   hidden_in   device [T][d], model dtype: the shared first-layer input X
+ *               (token + position embeddings, Section 3.1), sequences packed
+ *               back to back with no padding.
+ *   cu_seqlens  HOST int32[num_seqs + 1]: cu[0] = 0, strictly increasing
+ *               (no empty sequence), T = cu[num_seqs] <= max_tokens.
+ *               Tokens cu[b] .. cu[b+1]-1 form sequence b; attention is
+ *               causal within a sequence and never crosses sequences.
+ *   num_seqs    1 .. KRAKEN_MAX_SEQS.
+ *   hidden_out  device float32 [T][d]: out = [Y_1|...|Y_N] W_concat.
+ *   sub_out     NULL or device float32 [N][T][d]: the final sub-layer
+ *               outputs Y_i before W_concat.
+ * Outputs are fp32 whatever the storage dtype (the residual stream and all
+ * accumulation are fp32).  Outputs must not overlap the input or each other.
+ * The call enqueues the whole pass on `stream` and returns; it keeps no
+ * pointer to caller memory.  One prefill at a time per model: concurrent
+ * calls on one model must be serialised by the caller (e.g. one stream).
+ * Errors: INVALID_ARG, STATE (weights not loaded), HIP.
+ */
+kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
+                             int32_t num_seqs, float* hidden_out, float* sub_out, void* stream);
+
+/* Waits for the model's device work, frees everything it owns.  NULL is a no-op. */
+kraken_status kraken_destroy(kraken_model* m);
+
+const char* kraken_status_string(kraken_status s);
+const char* kraken_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Per-kernel timing of kraken_prefill (measurement support).
+ * When enabled, every launch of a prefill is bracketed by a pair of HIP
+ * events on the prefill's stream; kraken_profile_read returns, per kernel
+ * class, the summed device time in ms and the number of launches since the
+ * last reset.  Reading waits for the recorded events.  Kernel classes:
+ */
+enum {
+  KRAKEN_K_LN1 = 0,        /* LayerNorm before MHA */
+  KRAKEN_K_GEMM_QK = 1,    /* Q,K projection */
+  KRAKEN_K_GEMM_VT = 2,    /* V projection (written transposed) */
+  KRAKEN_K_ATTN = 3,       /* causal flash attention */
+  KRAKEN_K_GEMM_O = 4,     /* output projection + residual */
+  KRAKEN_K_COMBINE = 5,    /* N-way sum + residual + LayerNorm before FFN */
+  KRAKEN_K_GEMM_UP = 6,    /* FFN up projection + GELU */
+  KRAKEN_K_GEMM_DOWN = 7,  /* FFN down projection + residual */
+  KRAKEN_K_CONCAT = 8,     /* W_concat (and its operand split) */
+  KRAKEN_K_OTHER = 9,      /* input conversion, output copies */
+  KRAKEN_K_COUNT = 10
+};
+kraken_status kraken_profile_enable(kraken_model* m, int enable);
+kraken_status kraken_profile_read(kraken_model* m, int kernel_class, double* total_ms,
+                                  int64_t* launches);
+kraken_status kraken_profile_reset(kraken_model* m);
+/* Algorithmic FLOPs (matrix products and attention, causal pairs only) of one
+ * prefill over `cu_seqlens`, per kernel class: returns 0 for classes that do
+ * no matrix work. */
+double kraken_class_flops(const kraken_config* cfg, int kernel_class, const int32_t* cu_seqlens,
+                          int32_t num_seqs);
+
+/* ------------------------------------------------------------------------
+ * Single-kernel entry points: the same kernels kraken_prefill launches, on
+ * caller buffers, for per-kernel parity tests.  All pointers are device
+ * pointers; `dtype` is a kraken_dtype naming the operand type "S" below.
+ *
+ * kraken_op_layernorm (Algorithm 1, LN1): out[i][t][:] = LN(x_i[t][:]; g_i, b_i)
+ *   x float32 at x + i*x_batch_stride + t*d (x_batch_stride may be 0: shared
+ *   input), g/b float32 [n][d], out S [n][T][d].
+ */
+kraken_status kraken_op_layernorm(int32_t dtype, const float* x, int64_t x_batch_stride,
+                                  const float* gamma, const float* beta, void* out,
+                                  int32_t n, int32_t T, int32_t d, float eps, void* stream);
+
+/*
+ * kraken_op_combine_ln2 (Algorithm 1, second LayerNorm; Section 3.1 combine):
+ *   y[t] = shared[t] if shared != NULL, else sum_k x[k][t]  (k < n)
+ *   out[i][t] = LN(h[i][t] + y[t]; g_i, b_i)
+ *   x, h float32 [n][T][d]; shared float32 [T][d] or NULL; out S [n][T][d].
+ */
+kraken_status kraken_op_combine_ln2(int32_t dtype, const float* x, const float* shared,
+                                    const float* h, const float* gamma, const float* beta,
+                                    void* out, int32_t n, int32_t T, int32_t d, float eps,
+                                    void* stream);
+
+/*
+ * kraken_op_gemm: batched C[z] = epilogue(A[z] B[z]^T), z < batch, with
+ *   A S [M][K] (row stride K, batch stride sA), B S [N][K] (row stride K,
+ *   batch stride sB), fp32 accumulation.  epilogue:
+ *     0  C = acc + bias[n]              C is S     (bias float32 [batch][N])
+ *     1  C = GELU(acc + bias[n])        C is S     (exact erf GELU)
+ *     2  C = acc + bias[n] + R[m][n]    C is float32, R float32 with batch
+ *                                       stride sR (may be 0)
+ *     3  C = acc + bias[m]              C is S     (bias float32 [batch][M])
+ *   Row stride of C and R is N; batch strides are in elements; bias may be
+ *   NULL (no bias).  K must be a multiple of 64 elements.
+ */
+kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, const void* B,
+                             void* C, const float* bias, const float* R, int32_t M, int32_t N,
+                             int32_t K, int32_t batch, int64_t sA, int64_t sB, int64_t sC,
+                             int64_t sR, void* stream);
+
+/*
+ * kraken_op_attention (Section 2.1, causal MHA core; packed sequences):
+ *   qk S [n][T][2d] (row t: Q then K, head h at columns h*hd of each half),
+ *   vt S [n][d][ldv] (V transposed: row c is feature c over tokens), with
+ *      ldv = T rounded up to a multiple of 64 (KRAKEN_VT_LD(T)),
+ *   out S [n][T][d]: out = softmax(Q K^T / sqrt(hd) + causal mask) V per head.
+ *   cu_seqlens is a HOST int32[num_seqs+1] array as in kraken_prefill.
+ */
+kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
+                                  int32_t n, int32_t d, int32_t n_heads,
+                                  const int32_t* cu_seqlens, int32_t num_seqs, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KRAKEN_H_ */

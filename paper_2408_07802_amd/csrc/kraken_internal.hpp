@@ -1,0 +1,120 @@
+// Internal declarations shared by the Kraken HIP kernels and the runtime.
+// Target: gfx950 (CDNA4), 64-lane wavefronts, MFMA matrix cores.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kraken {
+
+typedef __bf16 bf16;
+typedef _Float16 f16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Element types.  For a model, the storage type is what the caller's weight blob and
+// input use; the compute type is the MFMA operand type of every GEMM and of attention.
+enum class DType : int { F32 = 0, BF16 = 1, F16 = 2 };
+
+inline size_t dtype_size(DType t) { return t == DType::F32 ? 4 : 2; }
+
+template <typename S>
+struct IsHalfWidth {
+  static constexpr bool value = sizeof(S) == 2;
+};
+
+// One 16-byte operand chunk per lane into a 32x32 MFMA block.
+// 16-bit types: the chunk is 8 consecutive k of the lane's row (k = 8*half + j), one
+//   v_mfma_f32_32x32x16_{bf16,f16}.
+// fp32: the chunk is 4 consecutive k; MFMA q (0..3) takes element q of both halves, so
+//   lane half h supplies k = 4*h + q, the same permutation of k for A and B.
+template <typename S>
+__device__ __forceinline__ f32x16 mfma_chunk(uint4 a, uint4 b, f32x16 c) {
+  if constexpr (__is_same(S, bf16)) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  } else if constexpr (__is_same(S, f16)) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  } else {
+    const f32x4 a4 = __builtin_bit_cast(f32x4, a), b4 = __builtin_bit_cast(f32x4, b);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], b4[q], c, 0, 0, 0);
+    return c;
+  }
+}
+
+// Epilogues of the batched GEMM C = epi(A B^T).
+enum GemmEpi : int {
+  EPI_BIAS_N = 0,       // C (storage type) = acc + bias[n]
+  EPI_BIAS_N_GELU = 1,  // C (storage type) = GELU(acc + bias[n]), exact erf form
+  EPI_BIAS_N_RES = 2,   // C (float32)      = acc + bias[n] + R[m][n]   (bias, R optional)
+  EPI_BIAS_M = 3        // C (storage type) = acc + bias[m]
+};
+
+// C[z][m][n] = epi( sum_g sum_k A[z][g][m][k] * B[z][g mod gBmod][n][k] )
+// A element (z,g,m,k) at A + z*sA + g*gA + m*lda + k; B likewise with ldb/sB/gB;
+// C element at C + z*sC + m*ldc + n; R at R + z*sR + m*ldc + n; bias at bias + z*sBias.
+struct GemmDesc {
+  DType dt;
+  int epi;
+  const void* A;
+  const void* B;
+  void* C;
+  const float* bias;
+  const float* R;
+  int M, N, K;  // K per group, multiple of 64 (bf16) / 32 (fp32)
+  int lda, ldb, ldc;
+  int64_t sA, sB, sC, sR, sBias;
+  int batch;
+  int kgroups;
+  int64_t gA, gB;
+  int gBmod;
+};
+
+hipError_t launch_gemm(const GemmDesc& g, hipStream_t s);
+
+// Causal flash attention over packed sequences.
+struct AttnDesc {
+  DType dt;
+  const void* qk;   // [n][T][2d]   (Q | K per row)
+  const void* vt;   // [n][d][T]    (V transposed)
+  void* out;        // [n][T][d]
+  int n, T, d, n_heads;
+  const int32_t* cu_host;  // host cu_seqlens [num_seqs + 1]
+  int num_seqs;
+};
+
+hipError_t launch_attention(const AttnDesc& a, hipStream_t s);
+
+// Row stride (elements) of the transposed V buffer for T tokens: a multiple of 64,
+// so that every 8-token group of a row starts on a 16-byte boundary.
+inline int vt_ld(int T) { return (T + 63) & ~63; }
+
+// LayerNorm of n rows-sets: out[i][t] = LN(x[i*xs + t*d]) with per-i gamma/beta.
+hipError_t launch_layernorm(DType dt, const float* x, int64_t x_batch_stride, const float* gamma,
+                            const float* beta, void* out, int n, int T, int d, float eps,
+                            hipStream_t s);
+
+// out[i][t] = LN(h[i][t] + y[t]); y = shared[t] or sum_k x[k][t].
+hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
+                              const float* gamma, const float* beta, void* out, int n, int T,
+                              int d, float eps, hipStream_t s);
+
+// dst[k] = float(src[k]) for k < count.
+hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, hipStream_t s);
+
+// Two-term split of fp32 values in a 16-bit type: hi = S(v), lo = S(v - hi);
+// hi at dst, lo at dst + count (elements).
+hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, hipStream_t s);
+
+// dst[c][r] = Dst(src[r*src_ld + c]) for r < R, c < C, dst row stride dst_ld.  When the
+// destination is fp16 and a finite source value does not fit, *overflow is set to 1.
+hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
+                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s);
+
+}  // namespace kraken

@@ -1,0 +1,293 @@
+// Bandwidth-bound kernels of the Kraken layer:
+//  * LN1: the LayerNorm in front of each sub-layer's attention (Algorithm 1);
+//  * combine + LN2: the element-wise sum of the previous layer's N sub-layer
+//    outputs (the paper's AllReduce, done on-device; Section 3.1), added to the
+//    sub-layer's residual and normalised in front of its FFN (Algorithm 1),
+//    in one pass over HBM;
+//  * conversions and the one-time weight transpose used at load.
+//
+// One workgroup owns one token: it reads the token's row of every sub-layer,
+// so each HBM byte is touched once.  Rows are read as float4, statistics are
+// kept in fp32 with a two-pass (mean, then centred variance) reduction.
+#include "kraken_internal.hpp"
+
+namespace kraken {
+namespace {
+
+constexpr int NORM_THREADS = 256;
+constexpr int MAX_VEC = 8;   // float4 per thread -> d <= 8192
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum over the workgroup; every thread gets the result.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();                     // red[] may still be read by a previous call
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < NORM_THREADS / 64; ++w) s += red[w];
+  return s;
+}
+
+template <typename S>
+__device__ __forceinline__ void store4(S* dst, float a, float b, float c, float d);
+
+template <>
+__device__ __forceinline__ void store4<float>(float* dst, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
+}
+
+template <>
+__device__ __forceinline__ void store4<bf16>(bf16* dst, float a, float b, float c, float d) {
+  bf16x4 v;
+  v[0] = (bf16)a; v[1] = (bf16)b; v[2] = (bf16)c; v[3] = (bf16)d;
+  *reinterpret_cast<bf16x4*>(dst) = v;
+}
+
+template <>
+__device__ __forceinline__ void store4<f16>(f16* dst, float a, float b, float c, float d) {
+  f16x4 v;
+  v[0] = (f16)a; v[1] = (f16)b; v[2] = (f16)c; v[3] = (f16)d;
+  *reinterpret_cast<f16x4*>(dst) = v;
+}
+
+// Normalise v (this thread's float4s of one row) and write the row to dst.
+template <typename S>
+__device__ __forceinline__ void ln_write(const float4* v, int nv, float mean, float rstd,
+                                         const float* gamma, const float* beta, S* dst) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < MAX_VEC; ++u) {
+    if (u >= nv) break;
+    const int c = (tid + u * NORM_THREADS) * 4;
+    const float4 g = *reinterpret_cast<const float4*>(gamma + c);
+    const float4 b = *reinterpret_cast<const float4*>(beta + c);
+    store4(dst + c, (v[u].x - mean) * rstd * g.x + b.x, (v[u].y - mean) * rstd * g.y + b.y,
+           (v[u].z - mean) * rstd * g.z + b.z, (v[u].w - mean) * rstd * g.w + b.w);
+  }
+}
+
+__device__ __forceinline__ void row_stats(const float4* v, int nv, int d, float eps,
+                                          float* red, float& mean, float& rstd) {
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < MAX_VEC; ++u)
+    if (u < nv) s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+  mean = block_sum(s, red) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int u = 0; u < MAX_VEC; ++u)
+    if (u < nv) {
+      const float a = v[u].x - mean, b = v[u].y - mean, c = v[u].z - mean, e = v[u].w - mean;
+      q += (a * a + b * b) + (c * c + e * e);
+    }
+  const float var = block_sum(q, red) / (float)d;
+  rstd = rsqrtf(var + eps);
+}
+
+// Number of float4s this thread owns in a row of d floats.
+__device__ __forceinline__ int my_vecs(int d) {
+  const int nv4 = d / 4;
+  const int tid = threadIdx.x;
+  return tid < nv4 ? (nv4 - tid + NORM_THREADS - 1) / NORM_THREADS : 0;
+}
+
+template <typename S>
+__global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
+    const float* __restrict__ x, int64_t xs, const float* __restrict__ gamma,
+    const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, float eps) {
+  __shared__ float red[NORM_THREADS / 64];
+  const int t = blockIdx.x;
+  const int nv = my_vecs(d);
+  float4 v[MAX_VEC];
+  float mean = 0.f, rstd = 0.f;
+  for (int i = 0; i < n; ++i) {
+    if (i == 0 || xs != 0) {
+      const float* row = x + i * xs + (int64_t)t * d;
+#pragma unroll
+      for (int u = 0; u < MAX_VEC; ++u)
+        if (u < nv) v[u] = *reinterpret_cast<const float4*>(row + (threadIdx.x + u * NORM_THREADS) * 4);
+      row_stats(v, nv, d, eps, red, mean, rstd);
+    }
+    ln_write(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
+             out + ((int64_t)i * T + t) * d);
+  }
+}
+
+template <typename S>
+__global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
+    const float* __restrict__ x, const float* __restrict__ shared, const float* __restrict__ h,
+    const float* __restrict__ gamma, const float* __restrict__ beta, S* __restrict__ out, int n,
+    int T, int d, float eps) {
+  __shared__ float red[NORM_THREADS / 64];
+  const int t = blockIdx.x;
+  const int nv = my_vecs(d);
+  const int64_t plane = (int64_t)T * d;
+  float4 y[MAX_VEC];
+  // y = X (first layer) or the N-way sum of the previous layer's outputs
+#pragma unroll
+  for (int u = 0; u < MAX_VEC; ++u) {
+    if (u >= nv) break;
+    const int c = (threadIdx.x + u * NORM_THREADS) * 4;
+    if (shared) {
+      y[u] = *reinterpret_cast<const float4*>(shared + (int64_t)t * d + c);
+    } else {
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int k = 0; k < n; ++k) {
+        const float4 b = *reinterpret_cast<const float4*>(x + k * plane + (int64_t)t * d + c);
+        a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+      }
+      y[u] = a;
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    float4 v[MAX_VEC];
+    const float* hrow = h + i * plane + (int64_t)t * d;
+#pragma unroll
+    for (int u = 0; u < MAX_VEC; ++u) {
+      if (u >= nv) break;
+      const float4 a = *reinterpret_cast<const float4*>(hrow + (threadIdx.x + u * NORM_THREADS) * 4);
+      v[u] = make_float4(a.x + y[u].x, a.y + y[u].y, a.z + y[u].z, a.w + y[u].w);
+    }
+    float mean, rstd;
+    row_stats(v, nv, d, eps, red, mean, rstd);
+    ln_write(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
+             out + (i * plane + (int64_t)t * d));
+  }
+}
+
+template <typename S>
+__global__ void to_f32_kernel(const S* __restrict__ src, float* __restrict__ dst, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < count; k += stride)
+    dst[k] = (float)src[k];
+}
+
+template <typename S>
+__global__ void split16_kernel(const float* __restrict__ src, S* __restrict__ dst, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < count; k += stride) {
+    const float v = src[k];
+    const S hi = (S)v;
+    dst[k] = hi;
+    dst[k + count] = (S)(v - (float)hi);
+  }
+}
+
+template <typename Src, typename Dst>
+__global__ __launch_bounds__(256) void transpose_kernel(const Src* __restrict__ src, int64_t sld,
+                                                        Dst* __restrict__ dst, int64_t dld, int R,
+                                                        int C, int* __restrict__ overflow) {
+  __shared__ float tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int k = ty; k < 64; k += 4) {
+    const int r = r0 + k, c = c0 + tx;
+    if (r < R && c < C) tile[k][tx] = (float)src[(int64_t)r * sld + c];
+  }
+  __syncthreads();
+  bool over = false;
+  for (int k = ty; k < 64; k += 4) {
+    const int c = c0 + k, r = r0 + tx;
+    if (r < R && c < C) {
+      const float v = tile[tx][k];
+      const Dst o = (Dst)v;
+      if constexpr (__is_same(Dst, f16)) over |= (__builtin_isinf((float)o) && !__builtin_isinf(v));
+      dst[(int64_t)c * dld + r] = o;
+    }
+  }
+  if (over && overflow) *overflow = 1;
+}
+
+unsigned grid_for(int64_t count) {
+  int64_t b = (count + 255) / 256;
+  if (b > 65536) b = 65536;
+  if (b < 1) b = 1;
+  return (unsigned)b;
+}
+
+template <class Fn>
+hipError_t by_type(DType dt, Fn&& fn) {
+  switch (dt) {
+    case DType::BF16: return fn(bf16{});
+    case DType::F16: return fn(f16{});
+    case DType::F32: return fn(float{});
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* gamma,
+                            const float* beta, void* out, int n, int T, int d, float eps,
+                            hipStream_t s) {
+  if (T <= 0 || n <= 0) return hipSuccess;
+  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(layernorm_kernel<S>, dim3(T), dim3(NORM_THREADS), 0, s, x, xs, gamma, beta,
+                       static_cast<S*>(out), n, T, d, eps);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
+                              const float* gamma, const float* beta, void* out, int n, int T,
+                              int d, float eps, hipStream_t s) {
+  if (T <= 0 || n <= 0) return hipSuccess;
+  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(combine_ln2_kernel<S>, dim3(T), dim3(NORM_THREADS), 0, s, x, shared, h,
+                       gamma, beta, static_cast<S*>(out), n, T, d, eps);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(to_f32_kernel<S>, dim3(grid_for(count)), dim3(256), 0, s,
+                       static_cast<const S*>(src), dst, count);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(split16_kernel<bf16>, dim3(grid_for(count)), dim3(256), 0, s, src,
+                       static_cast<bf16*>(dst), count);
+  else if (dt == DType::F16)
+    hipLaunchKernelGGL(split16_kernel<f16>, dim3(grid_for(count)), dim3(256), 0, s, src,
+                       static_cast<f16*>(dst), count);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
+                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s) {
+  if (R <= 0 || C <= 0) return hipSuccess;
+  dim3 grid((C + 63) / 64, (R + 63) / 64), block(256);
+  return by_type(src_t, [&](auto stag) {
+    using Src = decltype(stag);
+    return by_type(dst_t, [&](auto dtag) {
+      using Dst = decltype(dtag);
+      hipLaunchKernelGGL((transpose_kernel<Src, Dst>), grid, block, 0, s,
+                         static_cast<const Src*>(src), src_ld, static_cast<Dst*>(dst), dst_ld, R,
+                         C, overflow);
+      return hipGetLastError();
+    });
+  });
+}
+
+}  // namespace kraken

@@ -1,0 +1,296 @@
+"""Thin Python binding of the Kraken C ABI (include/kraken.h).
+
+Argument marshalling only: every step of the prefill runs in the HIP kernels of
+``libkraken.so``.  torch provides device memory and the current stream.  If the
+library has not been built this module raises instead of falling back to
+anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Iterable, List, Mapping, Optional, Sequence, Tuple
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkraken.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OOM, ERR_STATE, ERR_HIP = range(6)
+DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
+COMPUTE_CODES = {"storage": 0, "f32": 1, "bf16": 2, "f16": 3}
+MAX_SEQS = 256
+
+# kernel classes of the per-kernel timer (kraken.h)
+K_LN1, K_GEMM_QK, K_GEMM_VT, K_ATTN, K_GEMM_O, K_COMBINE, K_GEMM_UP, K_GEMM_DOWN, K_CONCAT, \
+    K_OTHER = range(10)
+K_COUNT = 10
+KERNEL_CLASS_NAMES = ["ln1", "gemm_qk", "gemm_vt", "attention", "gemm_o", "combine_ln2",
+                      "gemm_up", "gemm_down", "w_concat", "other"]
+
+EPI_BIAS_N, EPI_BIAS_N_GELU, EPI_BIAS_N_RES, EPI_BIAS_M = range(4)
+
+# Order of one sub-layer's tensors in the weight blob (kraken_load_weights).
+BLOB_ORDER = ("ln1_g", "ln1_b", "Wqkv", "bqkv", "Wo", "bo",
+              "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
+
+
+class KrakenError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"kraken status {status}: {msg}")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("n_sub", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("d_ff", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libkraken.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2408_07802_amd.build` (or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    fp = ctypes.c_float
+    P = ctypes.POINTER
+    sigs = {
+        "kraken_create": ([P(_Config), P(vp)], i32),
+        "kraken_weight_blob_elems": ([P(_Config)], sz),
+        "kraken_load_weights": ([vp, vp, sz, ctypes.c_int, vp], i32),
+        "kraken_prefill": ([vp, vp, P(i32), i32, vp, vp, vp], i32),
+        "kraken_destroy": ([vp], i32),
+        "kraken_status_string": ([i32], ctypes.c_char_p),
+        "kraken_last_error": ([], ctypes.c_char_p),
+        "kraken_profile_enable": ([vp, ctypes.c_int], i32),
+        "kraken_profile_read": ([vp, ctypes.c_int, P(ctypes.c_double), P(i64)], i32),
+        "kraken_profile_reset": ([vp], i32),
+        "kraken_class_flops": ([P(_Config), ctypes.c_int, P(i32), i32], ctypes.c_double),
+        "kraken_op_layernorm": ([i32, vp, i64, vp, vp, vp, i32, i32, i32, fp, vp], i32),
+        "kraken_op_combine_ln2": ([i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, fp, vp], i32),
+        "kraken_op_gemm": ([i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, i64, i64, i64,
+                            vp], i32),
+        "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, P(i32), i32, vp], i32),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise KrakenError(status, lib().kraken_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+def _cu_array(cu: Sequence[int]):
+    arr = (ctypes.c_int32 * len(cu))(*[int(v) for v in cu])
+    return arr
+
+
+def cu_from_lens(seq_lens: Sequence[int]) -> List[int]:
+    cu = [0]
+    for s in seq_lens:
+        cu.append(cu[-1] + int(s))
+    return cu
+
+
+def dtype_code(dtype) -> int:
+    if dtype in ("bf16", torch.bfloat16):
+        return DTYPE_BF16
+    if dtype in ("f16", torch.float16):
+        return DTYPE_F16
+    if dtype in ("f32", torch.float32):
+        return DTYPE_F32
+    raise ValueError(f"unsupported dtype {dtype!r}")
+
+
+def torch_dtype(code: int) -> torch.dtype:
+    return {DTYPE_BF16: torch.bfloat16, DTYPE_F16: torch.float16, DTYPE_F32: torch.float32}[code]
+
+
+@dataclasses.dataclass
+class Config:
+    n_sub: int
+    n_layers: int
+    d_model: int
+    n_heads: int
+    d_ff: int = 0
+    max_tokens: int = 1
+    dtype: str = "bf16"          # storage type of the weight blob and the input
+    compute: str = "storage"     # MFMA operand type: "storage", "f32", "bf16" or "f16"
+    ln_eps: float = 0.0
+
+    def c_struct(self) -> _Config:
+        return _Config(self.n_sub, self.n_layers, self.d_model, self.n_heads, self.d_ff,
+                       self.max_tokens, dtype_code(self.dtype), COMPUTE_CODES[self.compute],
+                       self.ln_eps)
+
+
+def weight_blob_elems(cfg: Config) -> int:
+    c = cfg.c_struct()
+    return int(lib().kraken_weight_blob_elems(ctypes.byref(c)))
+
+
+def class_flops(cfg: Config, kernel_class: int, cu: Sequence[int]) -> float:
+    c = cfg.c_struct()
+    return float(lib().kraken_class_flops(ctypes.byref(c), kernel_class, _cu_array(cu),
+                                          len(cu) - 1))
+
+
+def pack_weights(layers: Iterable[Sequence[Mapping[str, torch.Tensor]]],
+                 w_concat: torch.Tensor, cfg: Config, device=None) -> torch.Tensor:
+    """Flattens per-(layer, sub-layer) tensors into the blob order of kraken_load_weights."""
+    dt = torch_dtype(dtype_code(cfg.dtype))
+    device = device if device is not None else w_concat.device
+    blob = torch.empty(weight_blob_elems(cfg), dtype=dt, device=device)
+    off = 0
+    for layer in layers:
+        for sub in layer:
+            for name in BLOB_ORDER:
+                t = sub[name].reshape(-1)
+                blob[off:off + t.numel()].copy_(t)
+                off += t.numel()
+    t = w_concat.reshape(-1)
+    blob[off:off + t.numel()].copy_(t)
+    off += t.numel()
+    if off != blob.numel():
+        raise ValueError(f"blob has {off} elements, expected {blob.numel()}")
+    return blob
+
+
+class Kraken:
+    """A Kraken model on the current HIP device (owns its device memory)."""
+
+    def __init__(self, cfg: Config):
+        self.cfg = cfg
+        self._c = cfg.c_struct()
+        h = ctypes.c_void_p()
+        _check(lib().kraken_create(ctypes.byref(self._c), ctypes.byref(h)))
+        self._h = h
+        self.dtype = torch_dtype(self._c.dtype)
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        return self._h
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) and self._h.value:
+            lib().kraken_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def blob_elems(self) -> int:
+        return int(lib().kraken_weight_blob_elems(ctypes.byref(self._c)))
+
+    def load_weights(self, blob: torch.Tensor, stream=None) -> None:
+        if blob.dtype != self.dtype or not blob.is_contiguous():
+            raise ValueError("blob must be a contiguous tensor of the model dtype")
+        is_dev = 1 if blob.is_cuda else 0
+        _check(lib().kraken_load_weights(self._h, blob.data_ptr(),
+                                         blob.numel() * blob.element_size(), is_dev,
+                                         _stream(stream)))
+
+    def prefill(self, hidden: torch.Tensor, cu_seqlens: Sequence[int],
+                out: Optional[torch.Tensor] = None, sub_out=False,
+                stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+        """Runs the prefill; returns (out [T, d] fp32, sub_out [N, T, d] fp32 or None)."""
+        T = int(cu_seqlens[-1])
+        d = self.cfg.d_model
+        if out is None:
+            out = torch.empty((T, d), dtype=torch.float32, device=hidden.device)
+        if sub_out is True:
+            sub_out = torch.empty((self.cfg.n_sub, T, d), dtype=torch.float32,
+                                  device=hidden.device)
+        elif sub_out is False:
+            sub_out = None
+        cu = _cu_array(cu_seqlens)
+        _check(lib().kraken_prefill(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
+                                    out.data_ptr(), _ptr(sub_out), _stream(stream)))
+        return out, sub_out
+
+    # ---- per-kernel timing
+    def profile_enable(self, on: bool = True) -> None:
+        _check(lib().kraken_profile_enable(self._h, 1 if on else 0))
+
+    def profile_reset(self) -> None:
+        _check(lib().kraken_profile_reset(self._h))
+
+    def profile_read(self) -> dict:
+        res = {}
+        for k in range(K_COUNT):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            _check(lib().kraken_profile_read(self._h, k, ctypes.byref(ms), ctypes.byref(n)))
+            res[KERNEL_CLASS_NAMES[k]] = (ms.value, n.value)
+        return res
+
+
+# ----------------------------------------------------------------------------- single ops
+
+def op_layernorm(x: torch.Tensor, x_batch_stride: int, gamma: torch.Tensor, beta: torch.Tensor,
+                 out: torch.Tensor, n: int, T: int, d: int, eps: float = 1e-5,
+                 stream=None) -> torch.Tensor:
+    _check(lib().kraken_op_layernorm(dtype_code(out.dtype), x.data_ptr(), x_batch_stride,
+                                     gamma.data_ptr(), beta.data_ptr(), out.data_ptr(), n, T, d,
+                                     eps, _stream(stream)))
+    return out
+
+
+def op_combine_ln2(x: Optional[torch.Tensor], shared: Optional[torch.Tensor], h: torch.Tensor,
+                   gamma: torch.Tensor, beta: torch.Tensor, out: torch.Tensor, n: int, T: int,
+                   d: int, eps: float = 1e-5, stream=None) -> torch.Tensor:
+    _check(lib().kraken_op_combine_ln2(dtype_code(out.dtype), _ptr(x), _ptr(shared),
+                                       h.data_ptr(), gamma.data_ptr(), beta.data_ptr(),
+                                       out.data_ptr(), n, T, d, eps, _stream(stream)))
+    return out
+
+
+def op_gemm(epilogue: int, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor,
+            bias: Optional[torch.Tensor], R: Optional[torch.Tensor], M: int, N: int, K: int,
+            batch: int, sA: int, sB: int, sC: int, sR: int = 0, stream=None) -> torch.Tensor:
+    _check(lib().kraken_op_gemm(dtype_code(A.dtype), epilogue, A.data_ptr(), B.data_ptr(),
+                                C.data_ptr(), _ptr(bias), _ptr(R), M, N, K, batch, sA, sB, sC,
+                                sR, _stream(stream)))
+    return C
+
+
+def vt_ld(T: int) -> int:
+    return (T + 63) // 64 * 64
+
+
+def op_attention(qk: torch.Tensor, vt: torch.Tensor, out: torch.Tensor, n: int, d: int,
+                 n_heads: int, cu_seqlens: Sequence[int], stream=None) -> torch.Tensor:
+    cu = _cu_array(cu_seqlens)
+    _check(lib().kraken_op_attention(dtype_code(qk.dtype), qk.data_ptr(), vt.data_ptr(),
+                                     out.data_ptr(), n, d, n_heads, cu, len(cu_seqlens) - 1,
+                                     _stream(stream)))
+    return out

@@ -1,0 +1,227 @@
+"""Per-kernel parity: each HIP kernel of the prefill, through its C-ABI entry point,
+against the fp64 oracle's pieces (or the plain definition of the op) on the same inputs."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import kraken_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def K():
+    from paper_2408_07802_amd import kraken
+    return kraken
+
+
+def tdt(name):
+    return {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[name]
+
+
+def f64(t):
+    return t.detach().double().cpu().numpy()
+
+
+def check_close(got, ref, dtype_name, what, rel_elem=None, rel_rms=None):
+    got, ref = np.asarray(got, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), what
+    rms = float(np.sqrt(np.mean(ref ** 2))) if ref.size else 0.0
+    if rel_elem is None:
+        rel_elem = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 1e-6}[dtype_name]
+    if rel_rms is None:
+        rel_rms = {"bf16": 2e-3, "f16": 2.5e-4, "f32": 2e-6}[dtype_name]
+    bound = rel_elem * np.abs(ref) + rel_rms * rms + 1e-30
+    bad = np.abs(got - ref) > bound
+    if bad.any():
+        idx = np.unravel_index(np.argmax(np.abs(got - ref) - bound), ref.shape)
+        raise AssertionError(f"{what}: {bad.sum()} elements out of bound; worst at {idx}: "
+                             f"got {got[idx]!r} ref {ref[idx]!r} bound {bound[idx]!r}")
+
+
+# ----------------------------------------------------------------------------- LayerNorm
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("n,T,d,shared", [(3, 37, 128, False), (2, 5, 2048, True),
+                                          (4, 130, 768, False), (1, 1, 64, False),
+                                          (2, 9, 8192, False), (8, 3, 2048, True)])
+def test_layernorm(dtype, n, T, d, shared):
+    g = torch.Generator(device="cpu").manual_seed(n * 1000 + T * 7 + d)
+    x = (torch.randn((1 if shared else n, T, d), generator=g) * 3 + 1.5).to(DEV)
+    gamma = (1 + 0.3 * torch.randn((n, d), generator=g)).to(DEV)
+    beta = (0.3 * torch.randn((n, d), generator=g)).to(DEV)
+    out = torch.full((n, T, d), float("nan"), dtype=tdt(dtype), device=DEV)
+    K().op_layernorm(x, 0 if shared else T * d, gamma, beta, out, n, T, d, 1e-5)
+    torch.cuda.synchronize()
+    xs, gs, bs = f64(x), f64(gamma), f64(beta)
+    for i in range(n):
+        ref = O.layer_norm(xs[0 if shared else i], gs[i], bs[i])
+        check_close(f64(out[i]), ref, dtype, f"layernorm sub-layer {i}")
+
+
+# ------------------------------------------------------------------- combine + LN2
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("n,T,d,shared", [(2, 64, 128, True), (2, 64, 128, False),
+                                          (4, 33, 768, False), (8, 17, 2048, False),
+                                          (1, 5, 1280, False), (3, 2, 4096, True)])
+def test_combine_ln2(dtype, n, T, d, shared):
+    g = torch.Generator(device="cpu").manual_seed(n * 31 + T + d)
+    x = torch.randn((n, T, d), generator=g).to(DEV)
+    h = torch.randn((n, T, d), generator=g).to(DEV) * 2
+    X = torch.randn((T, d), generator=g).to(DEV) if shared else None
+    gamma = (1 + 0.3 * torch.randn((n, d), generator=g)).to(DEV)
+    beta = (0.3 * torch.randn((n, d), generator=g)).to(DEV)
+    out = torch.full((n, T, d), float("nan"), dtype=tdt(dtype), device=DEV)
+    K().op_combine_ln2(None if shared else x, X, h, gamma, beta, out, n, T, d, 1e-5)
+    torch.cuda.synchronize()
+    y = f64(X) if shared else f64(x).sum(axis=0)
+    hs, gs, bs = f64(h), f64(gamma), f64(beta)
+    for i in range(n):
+        ref = O.layer_norm(hs[i] + y, gs[i], bs[i])
+        check_close(f64(out[i]), ref, dtype, f"combine_ln2 sub-layer {i}")
+
+
+# ----------------------------------------------------------------------------- GEMM
+
+GEMM_SHAPES = [  # (M, N, K, batch)
+    (128, 128, 64, 1), (200, 96, 128, 2), (1, 300, 64, 1), (333, 129, 192, 3),
+    (64, 1536, 768, 2), (257, 2048, 256, 1), (1000, 64, 3072, 1),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_gemm(dtype, epi, shape):
+    M, N, Kd, batch = shape
+    g = torch.Generator(device="cpu").manual_seed(M * 7 + N * 3 + Kd + batch + epi * 101)
+    dt = tdt(dtype)
+    A = (torch.randn((batch, M, Kd), generator=g)).to(dt).to(DEV)
+    B = (torch.randn((batch, N, Kd), generator=g) * (1.0 / math.sqrt(Kd))).to(dt).to(DEV)
+    nb = M if epi == 3 else N
+    bias = (0.5 * torch.randn((batch, nb), generator=g)).to(DEV)
+    R = torch.randn((batch, M, N), generator=g).to(DEV) if epi == 2 else None
+    out_dt = torch.float32 if epi == 2 else dt
+    C = torch.full((batch, M, N), float("nan"), dtype=out_dt, device=DEV)
+    K().op_gemm(epi, A, B, C, bias, R, M, N, Kd, batch, M * Kd, N * Kd, M * N, M * N)
+    torch.cuda.synchronize()
+    a, b, bi = f64(A), f64(B), f64(bias)
+    for z in range(batch):
+        acc = a[z] @ b[z].T
+        if epi == 0:
+            ref = acc + bi[z][None, :]
+        elif epi == 1:
+            ref = O.gelu(acc + bi[z][None, :])
+        elif epi == 2:
+            ref = acc + bi[z][None, :] + f64(R[z])
+        else:
+            ref = acc + bi[z][:, None]
+        odt = "f32" if epi == 2 else dtype
+        # fp32 outputs of bf16 products: only accumulation-order error remains
+        kw = {"rel_elem": 1e-5, "rel_rms": 1e-5} if odt == "f32" else {}
+        check_close(f64(C[z]), ref, odt, f"gemm epi={epi} batch {z}", **kw)
+
+
+def test_gemm_without_bias_or_residual():
+    M, N, Kd = 70, 130, 128
+    g = torch.Generator(device="cpu").manual_seed(3)
+    A = torch.randn((M, Kd), generator=g).to(torch.bfloat16).to(DEV)
+    B = torch.randn((N, Kd), generator=g).to(torch.bfloat16).to(DEV)
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    K().op_gemm(2, A, B, C, None, None, M, N, Kd, 1, 0, 0, 0, 0)
+    torch.cuda.synchronize()
+    check_close(f64(C), f64(A) @ f64(B).T, "f32", "gemm plain", rel_elem=1e-5, rel_rms=1e-5)
+
+
+def test_gemm_shared_residual_batch_stride_zero():
+    M, N, Kd, batch = 50, 64, 64, 3
+    g = torch.Generator(device="cpu").manual_seed(4)
+    A = torch.randn((batch, M, Kd), generator=g).to(torch.bfloat16).to(DEV)
+    B = torch.randn((batch, N, Kd), generator=g).to(torch.bfloat16).to(DEV)
+    R = torch.randn((M, N), generator=g).to(DEV)
+    C = torch.empty((batch, M, N), dtype=torch.float32, device=DEV)
+    K().op_gemm(2, A, B, C, None, R, M, N, Kd, batch, M * Kd, N * Kd, M * N, 0)
+    torch.cuda.synchronize()
+    for z in range(batch):
+        check_close(f64(C[z]), f64(A[z]) @ f64(B[z]).T + f64(R), "f32", f"gemm shared R {z}",
+                    rel_elem=1e-5, rel_rms=1e-5)
+
+
+# ----------------------------------------------------------------------------- attention
+
+ATTN_CASES = [  # (n, d, heads, seq_lens)
+    (1, 128, 4, [64]), (2, 128, 4, [1, 7, 64, 5]), (2, 256, 4, [300]),
+    (1, 256, 2, [129, 1, 250]), (3, 768, 12, [200, 57]), (1, 512, 4, [513]),
+    (2, 2048, 16, [130]), (1, 1280, 20, [31, 97, 160]),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("case", ATTN_CASES)
+def test_attention(dtype, case):
+    n, d, H, lens = case
+    cu = [0]
+    for s in lens:
+        cu.append(cu[-1] + s)
+    T = cu[-1]
+    ldv = K().vt_ld(T)
+    dt = tdt(dtype)
+    g = torch.Generator(device="cpu").manual_seed(T * 13 + d + n)
+    qk = (torch.randn((n, T, 2 * d), generator=g) * 1.5).to(dt).to(DEV)
+    v = torch.randn((n, T, d), generator=g).to(dt)
+    vt = torch.zeros((n, d, ldv), dtype=dt)
+    vt[:, :, :T] = v.transpose(1, 2)
+    vt = vt.to(DEV)
+    out = torch.full((n, T, d), float("nan"), dtype=dt, device=DEV)
+    K().op_attention(qk, vt, out, n, d, H, cu)
+    torch.cuda.synchronize()
+    q64, v64 = f64(qk), f64(v)
+    for i in range(n):
+        ref = O.causal_attention(q64[i][:, :d], q64[i][:, d:], v64[i], cu, H)
+        check_attention(f64(out[i]), ref, q64[i], np.abs(v64[i]), cu, H, dtype,
+                        f"attention sub-layer {i}")
+
+
+def check_attention(got, ref, qk64, vabs, cu, H, dtype, what):
+    """Elementwise bound from the rounding model of the kernel.
+
+    bf16: the probabilities p are rounded to bf16 (relative error <= 2^-8) before the
+    P V product and the output is rounded to bf16, so
+    |err| <= 2^-8 (sum_k p_k |v_k| + |out|) plus fp32 accumulation error; the sum is
+    the oracle's attention applied to |V|.  fp32: the score error (fp32 dot products of
+    up to 128 terms, |s| up to ~30) moves each p by a relative ~1e-6 |s| through the
+    exponential; 2^-16 covers it.
+    """
+    d = qk64.shape[1] // 2
+    weighted_abs = O.causal_attention(qk64[:, :d], qk64[:, d:], vabs, cu, H)
+    u = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 2.0 ** -16}[dtype]
+    bound = u * (weighted_abs + np.abs(ref)) + 1e-6 * np.sqrt(np.mean(ref ** 2))
+    assert np.all(np.isfinite(got)), what
+    bad = np.abs(got - ref) > bound
+    if bad.any():
+        idx = np.unravel_index(np.argmax(np.abs(got - ref) / bound), ref.shape)
+        raise AssertionError(f"{what}: {bad.sum()} elements out of bound; worst at {idx}: "
+                             f"got {got[idx]!r} ref {ref[idx]!r} bound {bound[idx]!r}")
+
+
+def test_attention_large_logits_stay_finite():
+    n, d, H, lens = 1, 256, 2, [200]
+    T = 200
+    ldv = K().vt_ld(T)
+    g = torch.Generator(device="cpu").manual_seed(9)
+    qk = (torch.randn((n, T, 2 * d), generator=g) * 6).to(torch.bfloat16).to(DEV)
+    v = torch.randn((n, T, d), generator=g).to(torch.bfloat16)
+    vt = torch.zeros((n, d, ldv), dtype=torch.bfloat16)
+    vt[:, :, :T] = v.transpose(1, 2)
+    out = torch.empty((n, T, d), dtype=torch.bfloat16, device=DEV)
+    K().op_attention(qk, vt.to(DEV), out, n, d, H, [0, T])
+    torch.cuda.synchronize()
+    ref = O.causal_attention(f64(qk[0])[:, :d], f64(qk[0])[:, d:], f64(v[0]), [0, T], H)
+    check_attention(f64(out[0]), ref, f64(qk[0]), np.abs(f64(v[0])), [0, T], H, "bf16",
+                    "attention large logits")

@@ -1,0 +1,254 @@
+"""End-to-end parity of kraken_prefill (through the C ABI) against the fp64 oracle.
+
+Metric: max |gpu - oracle| / RMS(oracle), over ``out`` [T, d] and ``sub_out``
+[N, T, d]; bound 2e-2 for bf16 storage and 1e-4 for fp32 storage.
+
+Small workloads are checked in full.  At the full benchmark sizes the oracle
+cannot run every token in a test's time, so it runs a causal prefix of every
+sequence (exact by causality and packing: earlier tokens never see later ones,
+sequences never see each other) at the full depth and width, and that is
+compared with the same rows of the full-length GPU run.
+"""
+
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import kraken_oracle as O
+from paper_2408_07802_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def K():
+    from paper_2408_07802_amd import kraken
+    return kraken
+
+
+def f64(t):
+    return t.detach().double().cpu().numpy()
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def cfg_of(w, T):
+    return K().Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
+                      n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=T, dtype=w.dtype,
+                      compute=w.compute)
+
+
+def build_model(w, T, seed=0, affine="plain"):
+    cfg = cfg_of(w, T)
+    model = K().Kraken(cfg)
+    layers = (synth.gen_layer(w, j, seed, DEV, affine) for j in range(w.n_layers))
+    blob = K().pack_weights(layers, synth.gen_w_concat(w, seed, DEV), cfg, device=DEV)
+    model.load_weights(blob)
+    torch.cuda.synchronize()
+    del blob
+    return model
+
+
+def oracle_layers(w, seed=0, affine="plain"):
+    for j in range(w.n_layers):
+        yield [{k: f64(v) for k, v in sub.items()}
+               for sub in synth.gen_layer(w, j, seed, DEV, affine)]
+
+
+def rel_err(got, ref):
+    ref = np.asarray(ref)
+    return float(np.max(np.abs(np.asarray(got) - ref)) / np.sqrt(np.mean(ref ** 2)))
+
+
+def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
+    """Full-length GPU prefill; oracle on all tokens, or on the first `prefix` of each seq."""
+    cu = synth.cu_seqlens(lens)
+    T = cu[-1]
+    say(f"[prefill parity] {w.name} compute={w.compute} lens={lens[:8]} T={T} affine={affine} "
+        f"prefix={prefix}")
+    model = build_model(w, T, seed, affine)
+    X = synth.gen_hidden(w, T, seed, DEV)
+    out, sub = model.prefill(X, cu, sub_out=True)
+    torch.cuda.synchronize()
+    model.close()
+    assert torch.isfinite(out).all() and torch.isfinite(sub).all()
+    if prefix is None:
+        rows = np.arange(T)
+        cu_o = cu
+    else:
+        rows = np.concatenate([np.arange(cu[b], cu[b] + min(prefix, lens[b]))
+                               for b in range(len(lens))])
+        cu_o = synth.cu_seqlens([min(prefix, s) for s in lens])
+    Xo = f64(X)[rows]
+    out_o, sub_o = O.kraken_prefill(Xo, cu_o, oracle_layers(w, seed, affine),
+                                    f64(synth.gen_w_concat(w, seed, DEV)), w.n_heads)
+    e_out = rel_err(f64(out)[rows], out_o)
+    e_sub = rel_err(f64(sub)[:, rows], sub_o)
+    say(f"    max|err|/rms: out {e_out:.3e}  sub_out {e_sub:.3e}  (bound {TOL[w.dtype]})")
+    assert e_out <= TOL[w.dtype], e_out
+    assert e_sub <= TOL[w.dtype], e_sub
+    return e_out, e_sub
+
+
+def small(name, **kw):
+    base = dict(name=name, n_sub=2, n_layers=2, d_model=128, n_heads=4, d_ff=512, dtype="bf16")
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+# --------------------------------------------------------------- small workloads, in full
+
+@pytest.mark.parametrize("affine", ["plain", "random"])
+def test_fp32_n2_l2_d128_s64(affine):
+    w = synth.workload("kraken-n2-l2-d128-h4-s64-f32")
+    run_and_compare(w, synth.seq_lens(w), affine=affine)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("affine", ["plain", "random"])
+def test_ragged_several_tiles(dtype, affine):
+    # head size 64, ragged lengths spanning several 128-query tiles and 64-key tiles
+    w = small("ragged-n3-l2-d256-h4", n_sub=3, d_model=256, n_heads=4, d_ff=1024, dtype=dtype)
+    run_and_compare(w, [1, 130, 77, 300], affine=affine)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_head_size_128_and_32(dtype):
+    w = small("n2-l3-d256-h2", n_sub=2, n_layers=3, d_model=256, n_heads=2, d_ff=512, dtype=dtype)
+    run_and_compare(w, [200, 33], affine="random")
+    w = small("n4-l2-d128-h4", n_sub=4, n_layers=2, d_model=128, n_heads=4, d_ff=256, dtype=dtype)
+    run_and_compare(w, [96], affine="random")
+
+
+def test_single_sub_layer_single_token():
+    w = small("n1-l2-d128-h2", n_sub=1, n_layers=2, d_model=128, n_heads=2, d_ff=256, dtype="f32")
+    run_and_compare(w, [1], affine="random")
+    run_and_compare(w, [1, 1, 1], affine="random")
+
+
+# ------------------------------------------------------- benchmark-size workloads, prefix
+
+def test_n4_l12_d768_s2048_prefix():
+    w = synth.workload("kraken-n4-l12-d768-h12-s2048-bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=384)
+
+
+def test_n4_l12_d768_s2048_random_affine_prefix():
+    w = synth.workload("kraken-n4-l12-d768-h12-s2048-bf16")
+    run_and_compare(w, synth.seq_lens(w), affine="random", prefix=192)
+
+
+def test_n4_l24_d1024_s4096_prefix():
+    w = synth.workload("kraken-n4-l24-d1024-h16-s4096-bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=192)
+
+
+def test_n8_l24_d2048_s8192_prefix():
+    w = synth.workload("kraken-n8-l24-d2048-h16-s8192-bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=96)
+
+
+def test_n4_l36_d1280_ragged8_prefix():
+    w = synth.workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=40)
+
+
+# ------------------------------------------------------------------- GPU invariants
+
+def test_run_to_run_bitwise_determinism_and_prefix_invariance():
+    w = small("det-n3-l2-d256-h4", n_sub=3, d_model=256, n_heads=4, d_ff=1024)
+    lens = [300]
+    model = build_model(w, 300, affine="random")
+    X = synth.gen_hidden(w, 300, 0, DEV)
+    out1, sub1 = model.prefill(X, [0, 300], sub_out=True)
+    out2, sub2 = model.prefill(X, [0, 300], sub_out=True)
+    outp, subp = model.prefill(X[:133].contiguous(), [0, 133], sub_out=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out2) and torch.equal(sub1, sub2)
+    # rows never depend on later tokens: the same kernels give the same bits on a prefix
+    assert torch.equal(outp, out1[:133]) and torch.equal(subp, sub1[:, :133])
+    model.close()
+
+
+def test_zero_model_closed_form():
+    w = small("zero-n3-l3-d128", n_sub=3, n_layers=3)
+    T = 70
+    cfg = cfg_of(w, T)
+    model = K().Kraken(cfg)
+    F, d = w.d_ff, w.d_model
+    zero = {"ln1_g": torch.ones(d), "ln1_b": torch.zeros(d), "Wqkv": torch.zeros(d, 3 * d),
+            "bqkv": torch.zeros(3 * d), "Wo": torch.zeros(d, d), "bo": torch.zeros(d),
+            "ln2_g": torch.ones(d), "ln2_b": torch.zeros(d), "W1": torch.zeros(d, F),
+            "b1": torch.zeros(F), "W2": torch.zeros(F, d), "b2": torch.zeros(d)}
+    zero = {k: v.to(torch.bfloat16).to(DEV) for k, v in zero.items()}
+    wc = synth.gen_w_concat(w, 0, DEV)
+    blob = K().pack_weights([[zero] * 3] * 3, wc, cfg, device=DEV)
+    model.load_weights(blob)
+    X = synth.gen_hidden(w, T, 0, DEV)
+    out, sub = model.prefill(X, [0, 30, 70], sub_out=True)
+    torch.cuda.synchronize()
+    for i in range(3):
+        assert torch.equal(sub[i], X.float())       # x_i = X exactly in the fp32 residual
+    wsum = sum(f64(wc)[i * d:(i + 1) * d] for i in range(3))
+    assert rel_err(f64(out), f64(X) @ wsum) <= 1e-3
+    model.close()
+
+
+def test_state_error_before_load():
+    w = small("state", n_sub=1)
+    model = K().Kraken(cfg_of(w, 8))
+    X = torch.zeros((8, 128), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(K().KrakenError) as ei:
+        model.prefill(X, [0, 8])
+    assert ei.value.status == K().ERR_STATE
+    model.close()
+
+
+def test_host_blob_load_matches_device_blob_load():
+    w = small("hostblob", n_sub=2, n_layers=2, d_model=256, n_heads=4, d_ff=512)
+    T = 100
+    cfg = cfg_of(w, T)
+    blob = K().pack_weights((synth.gen_layer(w, j, 0, DEV, "random") for j in range(2)),
+                            synth.gen_w_concat(w, 0, DEV), cfg, device=DEV)
+    m1, m2 = K().Kraken(cfg), K().Kraken(cfg)
+    m1.load_weights(blob)
+    m2.load_weights(blob.cpu())
+    X = synth.gen_hidden(w, T, 0, DEV)
+    o1, _ = m1.prefill(X, [0, T])
+    o2, _ = m2.prefill(X, [0, T])
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    m1.close()
+    m2.close()
+
+
+def test_bf16_operands_n4_l12_d768_prefix():
+    # bf16 MFMA operands (no fp16 conversion): within the bound at this depth
+    w = dataclasses.replace(synth.workload("kraken-n4-l12-d768-h12-s2048-bf16"), compute="bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=256)
+
+
+def test_fp16_operand_overflow_is_rejected_at_load():
+    w = small("overflow", n_sub=1, compute="f16")
+    cfg = cfg_of(w, 8)
+    layer = synth.gen_layer(w, 0, 0, DEV)
+    layer[0]["W1"][3, 5] = 1.0e5                  # representable in bf16, not in fp16
+    blob = K().pack_weights([layer, synth.gen_layer(w, 1, 0, DEV)],
+                            synth.gen_w_concat(w, 0, DEV), cfg, device=DEV)
+    model = K().Kraken(cfg)
+    with pytest.raises(K().KrakenError) as ei:
+        model.load_weights(blob)
+    assert ei.value.status == K().ERR_UNSUPPORTED
+    X = torch.zeros((8, 128), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(K().KrakenError) as ei:      # the model stays unloaded
+        model.prefill(X, [0, 8])
+    assert ei.value.status == K().ERR_STATE
+    model.close()
