@@ -1,0 +1,205 @@
+"""Throughput benchmark of the Kraken prefill on one MI355X.
+
+One step = one kraken_prefill over the whole stack (L layers x N sub-layers, then
+W_concat) for one batch of synthetic input already resident in HBM.  Prints one
+JSON line: tokens/s and TTFT, the whole-path MFMA utilisation, a roofline entry for
+the dominant kernel (algorithmic FLOPs per launch over its average launch duration,
+from HIP events recorded around every launch on the prefill's stream during the
+timed steps), and the fp64 oracle timed on a bounded sample on the host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--compute f16|bf16] [--no-cpu-baseline]
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}   # MI355X dense
+METRIC = "prefill tokens/s + TTFT ms (all N sub-layers, 1 MI355X); MFMA util %"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, T, seed=0):
+    """The oracle on one sub-layer of one layer at the full sequence length.
+
+    All N x L sub-layers of a stack cost the same, so the stack's oracle time is the
+    sample's time x N x L (W_concat, 0.3% of the work, is left out of the sample).
+    """
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import kraken_oracle as O
+    from paper_2408_07802_amd import synth
+
+    p = {k: v.double().numpy() for k, v in synth.gen_sub_layer(w, 1, 0, seed, "cpu").items()}
+    x = synth.gen_hidden(w, T, seed, "cpu").double().numpy()
+    y = x * float(w.n_sub)          # any combine input: the cost does not depend on it
+    cu = [0, T]
+    t0 = time.perf_counter()
+    O.sub_layer_forward(x, y, p, cu, w.n_heads)
+    dt = time.perf_counter() - t0
+    stack_s = dt * w.n_sub * w.n_layers
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": T / stack_s, "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"1 of {w.n_sub} sub-layers x 1 of {w.n_layers} layers at the full "
+                      f"{T}-token length ({dt:.1f} s, fp64 numpy), extrapolated x"
+                      f"{w.n_sub * w.n_layers}",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--compute", default=None, help="MFMA operand type (default: workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the N sub-layers would shard across GPUs)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import dataclasses
+
+    import torch
+
+    from paper_2408_07802_amd import kraken, synth
+
+    w = synth.workload(args.workload or synth.BENCH_WORKLOAD)
+    if args.compute:
+        w = dataclasses.replace(w, compute=args.compute)
+    compute = w.dtype if w.compute == "storage" else w.compute
+    lens = synth.seq_lens(w)
+    cu = synth.cu_seqlens(lens)
+    T = cu[-1]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+
+    cfg = kraken.Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
+                        n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=T, dtype=w.dtype,
+                        compute=w.compute)
+    log(f"[bench] workload {w.name} T={T} compute={compute}: generating weights on device")
+    model = kraken.Kraken(cfg)
+    blob = kraken.pack_weights((synth.gen_layer(w, j, 0, dev) for j in range(w.n_layers)),
+                               synth.gen_w_concat(w, 0, dev), cfg, device=dev)
+    model.load_weights(blob)
+    torch.cuda.synchronize()
+    del blob
+    torch.cuda.empty_cache()
+    X = synth.gen_hidden(w, T, 0, dev)
+    out = torch.empty((T, w.d_model), dtype=torch.float32, device=dev)
+    log("[bench] weights loaded; warming up")
+
+    for _ in range(args.warmup):
+        model.prefill(X, cu, out=out)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps, no instrumentation
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        model.prefill(X, cu, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall / args.steps * 1e3:.3f})")
+
+    # ---- per-kernel durations: the same K steps with HIP events around every launch
+    model.profile_reset()
+    model.profile_enable(True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        model.prefill(X, cu, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_instr = ev0.elapsed_time(ev1) / args.steps
+    prof = model.profile_read()
+    model.profile_enable(False)
+
+    peak = MFMA_PEAK_TFLOPS[compute]
+    total_flops = sum(kraken.class_flops(cfg, k, cu) for k in range(kraken.K_COUNT))
+    kernels = {}
+    for k, name in enumerate(kraken.KERNEL_CLASS_NAMES):
+        ms, n = prof[name]
+        if n == 0:
+            continue
+        fl = kraken.class_flops(cfg, k, cu)
+        per_launch = fl / (n / args.steps) if fl else 0.0
+        avg_ms = ms / n
+        kernels[name] = {"ms_per_step": ms / args.steps, "launches_per_step": n // args.steps,
+                         "avg_launch_ms": avg_ms,
+                         "tflops": (per_launch / (avg_ms * 1e-3) / 1e12) if fl else None}
+    dominant = max((k for k in kernels if kernels[k]["tflops"] is not None),
+                   key=lambda k: kernels[k]["ms_per_step"])
+    dk = kernels[dominant]
+    gemm_names = ["gemm_qk", "gemm_vt", "gemm_o", "gemm_up", "gemm_down", "w_concat"]
+    gemm_ms = sum(kernels[k]["ms_per_step"] for k in gemm_names if k in kernels)
+    gemm_fl = sum(kraken.class_flops(cfg, kraken.KERNEL_CLASS_NAMES.index(k), cu)
+                  for k in gemm_names)
+    attn_ms = kernels["attention"]["ms_per_step"]
+    attn_fl = kraken.class_flops(cfg, kraken.K_ATTN, cu)
+
+    result = {
+        "metric": METRIC,
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "ttft_ms": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": compute,
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_sub": w.n_sub, "n_layers": w.n_layers,
+                   "d_model": w.d_model, "n_heads": w.n_heads, "d_ff": w.d_ff,
+                   "seq_lens": lens, "tokens": T, "storage_dtype": w.dtype,
+                   "mfma_operands": compute, "accumulate": "f32"},
+        "mfma_util_pct": 100.0 * total_flops / (ms_per_step * 1e-3) / (peak * 1e12),
+        "phase_mfma_util_pct": {
+            "gemm": 100.0 * gemm_fl / (gemm_ms * 1e-3) / (peak * 1e12),
+            "attention": 100.0 * attn_fl / (attn_ms * 1e-3) / (peak * 1e12)},
+        "algorithmic_tflop_per_step": total_flops / 1e12,
+        "roofline": {"bound": "mfma", "kernel": dominant,
+                     "achieved": dk["tflops"], "peak": peak, "unit": "TFLOP/s",
+                     "frac": dk["tflops"] / peak, "traffic": None,
+                     "avg_launch_ms": dk["avg_launch_ms"],
+                     "launches_per_step": dk["launches_per_step"]},
+        "kernels": kernels,
+        "instrumented_ms_per_step": ms_instr,
+        "wall_ms_per_step": wall / args.steps * 1e3,
+    }
+    model.close()
+    del X, out
+    torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on its sample")
+        result["cpu_baseline"] = cpu_baseline(w, T)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
