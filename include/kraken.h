@@ -245,7 +245,8 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
  * kraken_op_attention (Section 2.1, causal MHA core; packed sequences):
  *   qk S [n][T][2d] (row t: Q then K, head h at columns h*hd of each half),
  *   vt S [n][d][ldv] (V transposed: row c is feature c over tokens), with
- *      ldv = T rounded up to a multiple of 64 (KRAKEN_VT_LD(T)),
+ *      ldv = T rounded up to a multiple of 64 (KRAKEN_VT_LD(T)); the padding
+ *      columns [T, ldv) must hold finite values (they meet zero probabilities),
  *   out S [n][T][d]: out = softmax(Q K^T / sqrt(hd) + causal mask) V per head.
  *   cu_seqlens is a HOST int32[num_seqs+1] array as in kraken_prefill.
  */

@@ -6,28 +6,33 @@
 // each half); vt [n][d][ldv] holds V transposed (feature-major), written that
 // way by the V projection so that V^T tiles are contiguous rows.
 //
-// Formulation (one wave = 32 queries): the wave computes the score tile
-// transposed, S^T = K Q^T, with 32x32 MFMA blocks.  In the MFMA result layout
-// a lane then owns one query (one column) and half of the keys, so the running
-// max / sum of the online softmax are per-lane values; only the max is
-// exchanged once per tile with the partner lane (lane ^ 32).  The output is
-// accumulated transposed, O^T = V^T P^T, whose columns are again the lane's
-// query, so the rescale by exp(m_old - m_new) is lane-local too.  P^T goes from
-// the S^T accumulator registers straight into the B operand of the second MFMA:
-// the k-order of that operand is a permutation of the keys, and the V^T
-// operand is read from LDS in the same permuted order.
+// Formulation: a wave owns 64 queries (two 32-query MFMA blocks) and computes
+// the score tile transposed, S^T = K Q^T.  In the MFMA result layout a lane
+// then owns one query (one column) and half of the keys, so the running max /
+// sum of the online softmax are per-lane values; only the max is exchanged
+// once per tile with the partner lane (lane ^ 32).  The output is accumulated
+// transposed, O^T = V^T P^T, whose columns are again the lane's query, so the
+// rescale by exp(m_old - m_new) is lane-local; the exponent base only moves when
+// a maximum outgrows it by more than 2^8, so rescales are rare.  P^T goes from the S^T accumulator registers straight into
+// the B operand of the second MFMA.  The K rows of each 32-row fragment are
+// read in an order that swaps bits 2 and 3 of the row index; then result
+// register r of lane half h holds key 16 (r / 8) + 8 h + r % 8, so the eight
+// keys a lane feeds to one P V MFMA are contiguous and the V^T operand is a
+// single 16-byte LDS read.
 //
-// Workgroup: 4 waves = 128 queries of one (sub-layer, head, sequence); K and
-// V^T tiles of 64 keys are staged in a double-buffered LDS ring shared by the
-// four waves.  Tiles are ordered heaviest (longest causal prefix) first.
+// Workgroup: 4 waves = 256 queries of one (sub-layer, head, sequence).  K and
+// V^T tiles of 64 keys are copied from HBM straight into a 3-stage LDS ring
+// (global_load_lds_dwordx4), two tiles ahead of the tile being computed.
+// Workgroups are ordered heaviest (longest causal prefix) first.
 #include "kraken_internal.hpp"
 #include "../../include/kraken.h"
 
 namespace kraken {
 namespace {
 
-constexpr int BQ = 128;   // queries per workgroup
-constexpr int BKV = 64;   // keys per tile
+constexpr int QW = 64;               // queries per wave
+constexpr int BQ = 4 * QW;           // queries per workgroup
+constexpr int BKV = 64;              // keys per tile
 constexpr int ATT_THREADS = 256;
 
 struct AttnParams {
@@ -40,43 +45,71 @@ struct AttnParams {
   int tile_prefix[KRAKEN_MAX_SEQS + 1];
 };
 
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// 16 bytes per lane from global memory into LDS at `lds` + 16 * lane; ordered by the
+// kernel's own s_waitcnt vmcnt + barrier (see the GEMM for why it is inline assembly).
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(l), "v"(g) : "memory", "m0");
+}
+
+// Key row read by fragment row r: bits 2 and 3 of r swapped.
+__device__ __forceinline__ int kperm(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+// 16-byte-chunk swizzle of K rows: distinct for the 8 rows one 8-lane group reads.
+__device__ __forceinline__ int ksw(int row) { return (row & 3) | ((row >> 1) & 4); }
+
 template <typename S>
 __device__ __forceinline__ void store_out4(S* dst, float a, float b, float c, float e);
-
 template <>
 __device__ __forceinline__ void store_out4<bf16>(bf16* dst, float a, float b, float c, float e) {
   bf16x4 v;
   v[0] = (bf16)a; v[1] = (bf16)b; v[2] = (bf16)c; v[3] = (bf16)e;
   *reinterpret_cast<bf16x4*>(dst) = v;
 }
-
 template <>
 __device__ __forceinline__ void store_out4<f16>(f16* dst, float a, float b, float c, float e) {
   f16x4 v;
   v[0] = (f16)a; v[1] = (f16)b; v[2] = (f16)c; v[3] = (f16)e;
   *reinterpret_cast<f16x4*>(dst) = v;
 }
-
 template <>
 __device__ __forceinline__ void store_out4<float>(float* dst, float a, float b, float c, float e) {
   *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, e);
 }
 
-template <typename S, int HD>
-__global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnParams p) {
-  constexpr int ES = sizeof(S);
-  constexpr int CHK = HD * ES / 16;           // 16-byte chunks per K row
-  constexpr int KSW = (CHK < 8 ? CHK : 8) - 1;  // swizzle mask for K rows
-  constexpr int VROWB = BKV * ES;             // bytes per V^T row (64 keys)
-  constexpr int VCH = VROWB / 16;             // 16-byte chunks per V^T row
-  constexpr int NQC = HD * ES / 32;           // chunk pairs per head row
-  constexpr int OB = HD / 32;                 // 32-row blocks of O^T
-  constexpr int KLOAD = BKV * CHK / ATT_THREADS;
-  constexpr int VLOAD = HD * VCH / ATT_THREADS;
-  constexpr int KBYTES = BKV * HD * ES;
-  static_assert(KLOAD >= 1 && VLOAD >= 1, "tile too small for the workgroup");
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
 
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2][2 * KBYTES];
+template <typename S, int HD>
+__global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
+  constexpr int ES = sizeof(S);
+  constexpr int EPC = 16 / ES;                // elements per 16-byte chunk
+  constexpr int CHK = HD * ES / 16;           // chunks per K row
+  constexpr int KSWM = (CHK < 8 ? CHK : 8) - 1;
+  constexpr int VCH = BKV * ES / 16;          // chunks per V^T row
+  constexpr int NQC = HD * ES / 32;           // chunk pairs per head row (MFMA k steps)
+  constexpr int OB = HD / 32;                 // 32-row blocks of O^T
+  constexpr int TILE = BKV * HD * ES;         // bytes of one K (or V^T) tile
+  constexpr int STAGE = 2 * TILE;
+  constexpr int STAGES = 3 * STAGE <= 144 * 1024 ? 3 : 2;
+  constexpr int KI = CHK / 4;                 // K DMA instructions per wave per tile
+  constexpr int VI = HD * VCH / 256;          // V^T DMA instructions per wave per tile
+  constexpr int NPT = KI + VI;                // DMA instructions per wave per tile
+  static_assert(KI >= 1 && VI >= 1, "tile too small for the workgroup");
+
+  __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
 
   // ---- which (sub-layer, head, sequence, query tile)
   const int i = blockIdx.x / p.n_heads;
@@ -93,13 +126,11 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnParams p) {
   const int seq_start = p.cu[b], seq_end = p.cu[b + 1];
   const int q0 = seq_start + qt * BQ;
   const int q_hi = min(q0 + BQ, seq_end);
-  const int kv_begin = seq_start & ~7;       // 16-byte aligned V^T rows
+  const int kv_begin = seq_start & ~7;       // 16-byte aligned V^T chunks
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lhalf = lane >> 5;
-  const int wq0 = q0 + wave * 32;
-  const int wq_last = min(wq0 + 31, q_hi - 1);
-  const int my_q = wq0 + lrow;
+  const int wq0 = q0 + wave * QW;
 
   const int64_t ld_qk = 2 * (int64_t)p.d;
   const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
@@ -107,195 +138,211 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnParams p) {
   const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.d + h * HD) * p.ldv;
 
   // ---- Q fragments (B operand of S^T = K Q^T): lane's query, chunk 2*kc + lhalf
-  uint4 qf[NQC];
-  {
-    const S* qrow = qkz + (int64_t)my_q * ld_qk + h * HD;
+  uint4 qf[2][NQC];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int q = wq0 + qb * 32 + lrow;
+    const S* qrow = qkz + (int64_t)min(q, p.T - 1) * ld_qk + h * HD;
 #pragma unroll
     for (int kc = 0; kc < NQC; ++kc)
-      qf[kc] = (my_q < q_hi) ? *reinterpret_cast<const uint4*>(qrow + (2 * kc + lhalf) * (16 / ES))
-                             : make_uint4(0, 0, 0, 0);
+      qf[qb][kc] = (q < q_hi) ? *reinterpret_cast<const uint4*>(qrow + (2 * kc + lhalf) * EPC)
+                              : make_uint4(0, 0, 0, 0);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-  // ---- global -> register -> LDS staging of one K tile and one V^T tile
-  uint4 rk[KLOAD], rv[VLOAD];
-  auto gload = [&](int kt0) {
+  // ---- DMA of one K tile and one V^T tile into stage `st`.
+  auto issue = [&](int kt0, int st) {
+    unsigned char* base = smem + st * STAGE;
 #pragma unroll
-    for (int u = 0; u < KLOAD; ++u) {
-      const int q = tid + u * ATT_THREADS, row = q / CHK, ch = q % CHK;
-      const int key = kt0 + row;
-      rk[u] = (key < q_hi) ? *reinterpret_cast<const uint4*>(Kbase + (int64_t)key * ld_qk + ch * (16 / ES))
-                           : make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < KI; ++u) {
+      const int ins = wave * KI + u;                       // 1 KB = 64 / CHK rows
+      const int row = ins * (64 / CHK) + lane / CHK;
+      const int pch = lane % CHK;
+      const int lch = pch ^ (ksw(row) & KSWM);
+      const int key = min(kt0 + row, p.T - 1);
+      dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
     }
 #pragma unroll
-    for (int u = 0; u < VLOAD; ++u) {
-      const int q = tid + u * ATT_THREADS, row = q / VCH, ch = q % VCH;
-      const int key = kt0 + ch * (16 / ES);
-      const S* src = Vbase + (int64_t)row * p.ldv + key;
-      if (key + 16 / ES <= q_hi) {
-        rv[u] = *reinterpret_cast<const uint4*>(src);
-      } else {
-        S tmp[16 / ES];
-#pragma unroll
-        for (int e = 0; e < 16 / ES; ++e) tmp[e] = (key + e < q_hi) ? src[e] : S(0.f);
-        rv[u] = __builtin_bit_cast(uint4, tmp);
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint4* Ks = reinterpret_cast<uint4*>(smem[buf]);
-    unsigned char* Vs = smem[buf] + KBYTES;
-#pragma unroll
-    for (int u = 0; u < KLOAD; ++u) {
-      const int q = tid + u * ATT_THREADS, row = q / CHK, ch = q % CHK;
-      Ks[row * CHK + (ch ^ (row & KSW))] = rk[u];
-    }
-#pragma unroll
-    for (int u = 0; u < VLOAD; ++u) {
-      const int q = tid + u * ATT_THREADS, row = q / VCH, ch = q % VCH;
-      if constexpr (ES == 2) {
-        // 8-byte units, unit index XOR (row & 15)
-        uint2* V8 = reinterpret_cast<uint2*>(Vs + row * VROWB);
-        const int u0 = 2 * ch, sw = row & 15;
-        V8[u0 ^ sw] = make_uint2(rv[u].x, rv[u].y);
-        V8[(u0 + 1) ^ sw] = make_uint2(rv[u].z, rv[u].w);
-      } else {
-        uint4* V16 = reinterpret_cast<uint4*>(Vs + row * VROWB);
-        V16[ch ^ (row & 7)] = rv[u];
-      }
+    for (int u = 0; u < VI; ++u) {
+      const int ins = wave * VI + u;                       // 1 KB = 64 / VCH rows
+      const int row = ins * (64 / VCH) + lane / VCH;
+      const int pch = lane % VCH;
+      const int lch = pch ^ (row & 7);
+      const int key = min(kt0 + lch * EPC, p.ldv - EPC);
+      dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
     }
   };
 
-  f32x16 oacc[OB];
+  f32x16 oacc[2][OB];
 #pragma unroll
-  for (int ob = 0; ob < OB; ++ob)
+  for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[ob][r] = 0.f;
-  float m_run = -1e30f, l_run = 0.f;
+    for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[qb][ob][r] = 0.f;
+  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
 
   const int n_tiles = (q_hi - kv_begin + BKV - 1) / BKV;
-  gload(kv_begin);
-  lstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < n_tiles) issue(kv_begin + t * BKV, t);
 
-  for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it & 1;
-    const int kt0 = kv_begin + it * BKV;
-    if (it + 1 < n_tiles) gload(kt0 + BKV);
+  for (int t = 0; t < n_tiles; ++t) {
+    // tile t is complete once at most the later prefetched tiles are outstanding
+    if (STAGES == 3 && t + 1 < n_tiles) wait_vmcnt<NPT>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (t + STAGES - 1 < n_tiles) issue(kv_begin + (t + STAGES - 1) * BKV, (t + STAGES - 1) % STAGES);
 
-    if (wq0 < q_hi && kt0 <= wq_last) {
-      const uint4* Ks = reinterpret_cast<const uint4*>(smem[buf]);
-      const unsigned char* Vs = smem[buf] + KBYTES;
-      // S^T for keys [kt0, kt0+64): two 32x32 blocks
-      f32x16 st[2];
+    const int kt0 = kv_begin + t * BKV;
+    const unsigned char* base = smem + (t % STAGES) * STAGE;
+    const uint4* Ks = reinterpret_cast<const uint4*>(base);
+    const uint4* Vs = reinterpret_cast<const uint4*>(base + TILE);
+
+    // skip the tile when none of this wave's queries sees any of its keys; inside a
+    // processed tile both query blocks run (a block that sees none of the keys gets
+    // all-masked scores, i.e. zero weights)
+    if (wq0 >= q_hi || kt0 > min(wq0 + QW - 1, q_hi - 1)) continue;
+
+    // S^T for keys [kt0, kt0 + 64): two 32-key blocks per query block
+    f32x16 st[2][2];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) st[sb][r] = 0.f;
-        const int row = sb * 32 + lrow;
-#pragma unroll
-        for (int kc = 0; kc < NQC; ++kc)
-          st[sb] = mfma_chunk<S>(Ks[row * CHK + ((2 * kc + lhalf) ^ (row & KSW))], qf[kc], st[sb]);
-      }
-      // scale, causal / sequence-start mask, online softmax (lane = one query)
-      const bool need_mask = (kt0 < seq_start) || (kt0 + BKV - 1 > wq0);
-      float mx = m_run;
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float s = st[sb][r] * p.scale_log2;
-          if (need_mask) {
-            const int key = kt0 + sb * 32 + (r >> 2) * 8 + lhalf * 4 + (r & 3);
-            if (key > my_q || key < seq_start) s = -INFINITY;
+        for (int r = 0; r < 16; ++r) st[qb][sb][r] = 0.f;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const int row = kperm(sb * 32 + lrow);
+#pragma unroll
+      for (int kc = 0; kc < NQC; ++kc) {
+        const uint4 a = Ks[row * CHK + ((2 * kc + lhalf) ^ (ksw(row) & KSWM))];
+        st[0][sb] = mfma_chunk<S>(a, qf[0][kc], st[0][sb]);
+        st[1][sb] = mfma_chunk<S>(a, qf[1][kc], st[1][sb]);
+      }
+    }
+
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int my_q = wq0 + qb * 32 + lrow;
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[qb][sb][r] *= p.scale_log2;
+      if ((kt0 < seq_start) || (kt0 + BKV - 1 > wq0 + qb * 32)) {
+        // keys outside [seq_start, my_q] get weight 0; register r holds key
+        // kt0 + 8 lhalf + off(r) with off(r) = 32 sb + 16 (r / 8) + r % 8, so the test is
+        // one unsigned range check per register
+        const int base = kt0 + 8 * lhalf;
+        const unsigned lo = (unsigned)(seq_start - base);
+        const unsigned span = (unsigned)(my_q - seq_start);
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const unsigned off = (unsigned)(sb * 32 + (r >> 3) * 16 + (r & 7));
+            st[qb][sb][r] = (off - lo <= span) ? st[qb][sb][r] : -INFINITY;
           }
-          st[sb][r] = s;
-          mx = fmaxf(mx, s);
-        }
+      }
+      float mx = m_run[qb];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[qb][sb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float alpha = exp2f(m_run - mx);
-      m_run = mx;
+      // The exponent base m_run is only moved when some lane's maximum exceeds it by
+      // more than 8 (log2 units): weights stay <= 2^8, exact in the fp32 sums and within
+      // the range of the 16-bit P operand, and the O rescale is rare.
+      if (__ballot(mx > m_run[qb] + 8.0f)) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - mx);
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[qb][ob][r] *= alpha;
+        m_run[qb] = mx;
+      }
       float lsum = 0.f;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = exp2f(st[sb][r] - mx);
-          st[sb][r] = e;
+          const float e = __builtin_amdgcn_exp2f(st[qb][sb][r] - m_run[qb]);
+          st[qb][sb][r] = e;
           lsum += e;
         }
-      l_run = l_run * alpha + lsum;
-#pragma unroll
-      for (int ob = 0; ob < OB; ++ob)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[ob][r] *= alpha;
+      l_run[qb] += lsum;
+    }
 
-      // O^T += V^T P^T
-      if constexpr (ES == 2) {
-        typedef S s8 __attribute__((ext_vector_type(8)));
-        uint4 pb[2][2];
+    // O^T += V^T P^T
+    if constexpr (ES == 2) {
+      typedef S s8 __attribute__((ext_vector_type(8)));
+      uint4 pb[2][2][2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
             s8 v;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) v[j] = (S)st[sb][8 * hh + j];
-            pb[sb][hh] = __builtin_bit_cast(uint4, v);
+            for (int j = 0; j < 8; ++j) v[j] = (S)st[qb][sb][8 * hh + j];
+            pb[qb][sb][hh] = __builtin_bit_cast(uint4, v);
           }
 #pragma unroll
-        for (int ob = 0; ob < OB; ++ob) {
-          const int m = ob * 32 + lrow;
-          const uint2* V8 = reinterpret_cast<const uint2*>(Vs + m * VROWB);
-          const int sw = m & 15;
+      for (int ob = 0; ob < OB; ++ob) {
+        const int m = ob * 32 + lrow;
 #pragma unroll
-          for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-              // k = 8*lhalf + j  <->  key = 32 sb + 16 hh + 8 (j / 4) + 4 lhalf + j % 4
-              const int u1 = 8 * sb + 4 * hh + lhalf;
-              const uint2 lo4 = V8[u1 ^ sw], hi4 = V8[(u1 + 2) ^ sw];
-              oacc[ob] = mfma_chunk<S>(make_uint4(lo4.x, lo4.y, hi4.x, hi4.y), pb[sb][hh],
-                                       oacc[ob]);
+          for (int hh = 0; hh < 2; ++hh) {
+            // k = 8 lhalf + j  <->  key 32 sb + 16 hh + 8 lhalf + j: one 16-byte chunk
+            const uint4 a = Vs[m * VCH + ((4 * sb + 2 * hh + lhalf) ^ (m & 7))];
+            oacc[0][ob] = mfma_chunk<S>(a, pb[0][sb][hh], oacc[0][ob]);
+            oacc[1][ob] = mfma_chunk<S>(a, pb[1][sb][hh], oacc[1][ob]);
+          }
+      }
+    } else {
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob) {
+        const int m = ob * 32 + lrow;
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            // registers 4g .. 4g+3 hold keys 32 sb + 16 (g/2) + 8 lhalf + 4 (g%2) + (0..3)
+            const int c = 8 * sb + 4 * (g >> 1) + 2 * lhalf + (g & 1);
+            const f32x4 a4 = __builtin_bit_cast(f32x4, Vs[m * VCH + (c ^ (m & 7))]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              oacc[0][ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[0][sb][4 * g + q],
+                                                                 oacc[0][ob], 0, 0, 0);
+              oacc[1][ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[1][sb][4 * g + q],
+                                                                 oacc[1][ob], 0, 0, 0);
             }
-        }
-      } else {
-#pragma unroll
-        for (int ob = 0; ob < OB; ++ob) {
-          const int m = ob * 32 + lrow;
-          const uint4* V16 = reinterpret_cast<const uint4*>(Vs + m * VROWB);
-#pragma unroll
-          for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              // registers r = 4g .. 4g+3 hold keys 32 sb + 8 g + 4 lhalf + (0..3)
-              const int c = 8 * sb + 2 * g + lhalf;
-              const f32x4 a4 = __builtin_bit_cast(f32x4, V16[c ^ (m & 7)]);
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                oacc[ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[sb][4 * g + q],
-                                                                 oacc[ob], 0, 0, 0);
-            }
-        }
+          }
       }
     }
-
-    if (it + 1 < n_tiles) lstore(buf ^ 1);
-    __syncthreads();
   }
 
-  // ---- normalise and write O (lane: query my_q, features ob*32 + (r/4)*8 + 4*lhalf + r%4)
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (wq0 < q_hi && my_q < q_hi) {
-    const float inv = 1.0f / l_tot;
-    S* orow = static_cast<S*>(p.out) + ((int64_t)i * p.T + my_q) * p.d + h * HD;
+  // ---- normalise and write O (lane: query, features ob*32 + (r/4)*8 + 4*lhalf + r%4)
 #pragma unroll
-    for (int ob = 0; ob < OB; ++ob)
+  for (int qb = 0; qb < 2; ++qb) {
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
+    const int my_q = wq0 + qb * 32 + lrow;
+    if (my_q < q_hi) {
+      const float inv = 1.0f / l_tot;
+      S* orow = static_cast<S*>(p.out) + ((int64_t)i * p.T + my_q) * p.d + h * HD;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int m = ob * 32 + g * 8 + lhalf * 4;
-        store_out4(orow + m, oacc[ob][4 * g] * inv, oacc[ob][4 * g + 1] * inv,
-                   oacc[ob][4 * g + 2] * inv, oacc[ob][4 * g + 3] * inv);
-      }
+      for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = ob * 32 + g * 8 + lhalf * 4;
+          store_out4(orow + m, oacc[qb][ob][4 * g] * inv, oacc[qb][ob][4 * g + 1] * inv,
+                     oacc[qb][ob][4 * g + 2] * inv, oacc[qb][ob][4 * g + 3] * inv);
+        }
+    }
   }
 }
 

@@ -95,6 +95,10 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s);
 // so that every 8-token group of a row starts on a 16-byte boundary.
 inline int vt_ld(int T) { return (T + 63) & ~63; }
 
+// Sets columns [c0, c1) of `rows` rows (row stride ld elements) to zero.
+hipError_t launch_zero_cols(DType dt, void* base, int64_t rows, int64_t ld, int c0, int c1,
+                            hipStream_t s);
+
 // LayerNorm of n rows-sets: out[i][t] = LN(x[i*xs + t*d]) with per-i gamma/beta.
 hipError_t launch_layernorm(DType dt, const float* x, int64_t x_batch_stride, const float* gamma,
                             const float* beta, void* out, int n, int T, int d, float eps,

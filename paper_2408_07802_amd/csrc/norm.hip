@@ -206,6 +206,14 @@ __global__ __launch_bounds__(256) void transpose_kernel(const Src* __restrict__ 
   if (over && overflow) *overflow = 1;
 }
 
+template <typename S>
+__global__ void zero_cols_kernel(S* __restrict__ base, int64_t rows, int64_t ld, int c0, int w) {
+  const int64_t total = rows * w;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += stride)
+    base[(k / w) * ld + c0 + (k % w)] = S(0.f);
+}
+
 unsigned grid_for(int64_t count) {
   int64_t b = (count + 255) / 256;
   if (b > 65536) b = 65536;
@@ -257,6 +265,18 @@ hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, h
     using S = decltype(tag);
     hipLaunchKernelGGL(to_f32_kernel<S>, dim3(grid_for(count)), dim3(256), 0, s,
                        static_cast<const S*>(src), dst, count);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_zero_cols(DType dt, void* base, int64_t rows, int64_t ld, int c0, int c1,
+                            hipStream_t s) {
+  if (rows <= 0 || c1 <= c0) return hipSuccess;
+  const int w = c1 - c0;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(zero_cols_kernel<S>, dim3(grid_for(rows * w)), dim3(256), 0, s,
+                       static_cast<S*>(base), rows, ld, c0, w);
     return hipGetLastError();
   });
 }

@@ -486,6 +486,11 @@ kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32
     X32 = m->X32;
   }
 
+  // Attention reads V^T in 16-byte chunks of 8 tokens; the padding columns [T, ldv) are
+  // only ever multiplied by zero probabilities but must hold finite values.
+  if (ldv > T)
+    RUN(KRAKEN_K_OTHER, launch_zero_cols(dt, m->vt, N * d, ldv, T, ldv, s), "V padding");
+
   for (int j = 0; j < m->L; ++j) {
     const LayerW& w = m->layers[j];
     const float* xin = j == 0 ? X32 : m->xbuf;   // sub-layer inputs x_i
