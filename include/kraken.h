@@ -80,7 +80,8 @@ typedef enum {
  *   d_model    d, width of one sub-layer; multiple of 64
  *   n_heads    heads per sub-layer; d / n_heads must be 32, 64 or 128
  *   d_ff       MLP width; 0 means 4 d (Section 2.1); multiple of 64
- *   max_tokens largest packed token count T a prefill may use (>= 1)
+ *   max_tokens largest packed token count T a prefill may use (>= 1; at most
+ *              4194304, and max_tokens * max(2 d, d_ff) * 4 < 2^31)
  *   dtype      a kraken_dtype: element type of the weight blob and of hidden_in
  *   compute    a kraken_compute: MFMA operand type (0 = same as dtype)
  *   ln_eps     LayerNorm epsilon; 0 means 1e-5

@@ -343,6 +343,10 @@ hipError_t launch_gemm(const GemmDesc& g, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0 || g.kgroups <= 0) return hipSuccess;
   const int bk = g.dt == DType::F32 ? 32 : 64;
   if (g.K <= 0 || g.K % bk != 0 || g.gBmod <= 0) return hipErrorInvalidValue;
+  // the kernel addresses operand rows of one batch entry / K group with 32-bit byte offsets
+  const int64_t es = (int64_t)dtype_size(g.dt);
+  if ((int64_t)g.M * g.lda * es >= (1ll << 31) || (int64_t)g.N * g.ldb * es >= (1ll << 31))
+    return hipErrorInvalidValue;
   // 256 x 256 tiles when they give at least two waves of workgroups over the 256 CUs,
   // else 128 x 128 (small token counts or narrow projections).
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.batch;

@@ -146,6 +146,9 @@ kraken_status validate_cfg(const kraken_config* c) {
     return fail(KRAKEN_ERR_UNSUPPORTED, "d_model and d_ff must be multiples of 64");
   if (c->d_model > 8192) return fail(KRAKEN_ERR_UNSUPPORTED, "d_model above 8192");
   if (c->max_tokens > (1 << 22)) return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens above 4194304");
+  // GEMM operands of one sub-layer are addressed with 32-bit byte offsets
+  if ((int64_t)c->max_tokens * std::max(2 * c->d_model, F) * 4 >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens * max(2 d_model, d_ff) too large");
   if (c->dtype < KRAKEN_DTYPE_F32 || c->dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
   if (c->compute < KRAKEN_COMPUTE_STORAGE || c->compute > KRAKEN_COMPUTE_F16)

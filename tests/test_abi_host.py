@@ -60,6 +60,7 @@ def _create_status(**kw):
     (dict(d_model=96, n_heads=3), 2),         # d not a multiple of 64
     (dict(d_model=1280, n_heads=4), 2),       # head size 320
     (dict(d_ff=100), 2), (dict(max_tokens=1 << 23), 2),
+    (dict(d_model=2048, n_heads=16, d_ff=8192, max_tokens=65536), 2),   # 32-bit GEMM offsets
 ])
 def test_create_rejects_bad_configs_before_allocating(kw, status):
     assert _create_status(**kw) == status
