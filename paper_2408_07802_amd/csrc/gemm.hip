@@ -16,10 +16,12 @@
 // 32 fp32 elements).  Operand tiles go from HBM straight into LDS with
 // global_load_lds_dwordx4 (no register staging) into the other half of a
 // double-buffered LDS ring while the MFMAs consume the current half.  Tile rows
-// are 128 bytes; 16-byte chunk c of row r is stored at chunk c ^ (r & 7), so the
-// 8 lanes that read one chunk column of 8 consecutive rows hit distinct banks.
-// The swizzle is applied on the load side: each lane of a DMA load writes the
-// next 16 bytes of LDS, so it fetches the logical chunk that belongs there.
+// are 128 bytes; 16-byte chunk c of row r is stored at chunk c ^ swz_key(r), which
+// keeps fragment reads free of bank conflicts.  The swizzle is applied on the load
+// side: each lane of a DMA load writes the next 16 bytes of LDS, so it fetches the
+// logical chunk that belongs there.  The main loop's instruction order is fixed by
+// hand (fragment reads and DMAs interleaved one per MFMA, one barrier per slice) so
+// that the single wave per SIMD keeps the matrix pipe busy.
 // Rows past M (or N) load a clamped in-bounds row; they only feed outputs that
 // are never stored.
 #include <type_traits>
@@ -87,20 +89,40 @@ __device__ __forceinline__ void store4<f16>(f16* p, float4 v) {
   *reinterpret_cast<f16x4*>(p) = o;
 }
 
-// Row-swizzled 16-byte chunk index inside a 128-byte tile row.
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 7); }
+// Swizzle of 16-byte chunks inside a 128-byte tile row: logical chunk k of row r sits at
+// physical chunk k ^ swz_key(r).  The key mixes bit 3 of the row into bits 0-2 so that the
+// 16 rows one ds_read_b128 serves per LDS cycle cover all 64 banks exactly once (rows r and
+// r + 8 would collide under the plain r & 7).
+__device__ __forceinline__ int swz_key(int row) { return (row ^ (row >> 3)) & 7; }
+
+template <int N>
+using I = std::integral_constant<int, N>;
+
+// Compile-time loop: f(I<B>{}), f(I<B+1>{}), ..., f(I<E-1>{}).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(I<B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// MFMA slot (in [lo, hi)) that item k of n evenly spread items issues after.
+__host__ __device__ constexpr int spread_slot(int k, int n, int lo, int hi) {
+  return lo + (k * (hi - lo)) / n;
+}
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 
-// One 16-byte-per-lane DMA from global memory into LDS at `lds` + 16 * lane
-// (global_load_lds_dwordx4 with the wave-uniform LDS address in M0).  It is issued from
-// inline assembly so that the compiler does not order later LDS reads of the *other*
+// One 16-byte-per-lane DMA from global memory into LDS: global_load_lds_dwordx4 with a
+// wave-uniform base address (SGPR pair), a per-lane 32-bit byte offset, and the
+// wave-uniform LDS destination in M0; lane i's 16 bytes land at M0 + 16 i.  It is issued
+// from inline assembly so that the compiler does not order later LDS reads of the *other*
 // stage behind it; the kernel orders it explicitly (s_waitcnt vmcnt(0) + barrier before
 // the stage is read).
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :: "s"(l), "v"(g) : "memory", "m0");
+__device__ __forceinline__ void dma16(uint32_t lds_addr, const void* base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds_addr), "v"(off), "s"(base) : "memory", "m0");
 }
 
 template <typename S, int BM, int BN, int EPI>
@@ -113,6 +135,13 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int AI = BM / 32, BI = BN / 32;    // DMA instructions per wave per slice
   constexpr int STAGE = (BM + BN) * CH;        // uint4 per LDS stage
+  constexpr int NCH = CH / 2;                  // 16-byte-per-lane K chunks per slice
+  constexpr int NM = FM * FN;                  // MFMA blocks per chunk
+  constexpr int NR = FM + FN;                  // fragment reads per chunk
+  constexpr int ND = AI + BI;                  // DMA instructions per wave per slice
+  constexpr int BAR = NM * 3 / 4;              // last-chunk MFMA slot of the barrier
+  constexpr int DCH = 2;                       // chunks the slice's DMAs spread over
+  static_assert(DCH < NCH && BAR < NM, "schedule slots out of range");
 
   __shared__ uint4 lds[2 * STAGE];
 
@@ -133,43 +162,64 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int lrow = lane & 31, lhalf = lane >> 5;
 
   const S* Az = static_cast<const S*>(p.A) + z * p.sA;
   const S* Bz = static_cast<const S*>(p.B) + z * p.sB;
 
-  // DMA source offsets: wave loads rows [wave*BM/4, +BM/4) of A in instructions of 8 rows;
-  // lane writes row 8u + lane/8, physical chunk lane%8, so it fetches logical chunk
-  // (lane % 8) ^ (lane / 8).
-  const int dchunk = ((lane & 7) ^ (lane >> 3)) * EPC;
-  // (32-bit offsets: the host guarantees rows * leading dimension < 2^31 per operand)
+  // DMA: wave loads rows [wave*BM/4, +BM/4) of the A tile (and likewise of B) in
+  // instructions of 8 rows; lane writes row 8u + lane/8 of that block at physical chunk
+  // lane%8, so it fetches the logical chunk that the swizzle puts there.  Byte offsets
+  // from the slice's base pointer fit 32 bits (the host rejects larger operands).
   uint32_t aoff[AI], boff[BI];
 #pragma unroll
   for (int u = 0; u < AI; ++u) {
-    const int m = min(m0 + wave * (BM / 4) + u * 8 + (lane >> 3), p.M - 1);
-    aoff[u] = (uint32_t)m * (uint32_t)p.lda + dchunk;
+    const int rl = wave * (BM / 4) + u * 8 + (lane >> 3);
+    const int m = min(m0 + rl, p.M - 1);
+    aoff[u] = ((uint32_t)m * (uint32_t)p.lda + (uint32_t)(((lane & 7) ^ swz_key(rl)) * EPC)) *
+              (uint32_t)sizeof(S);
   }
 #pragma unroll
   for (int u = 0; u < BI; ++u) {
-    const int n = min(n0 + wave * (BN / 4) + u * 8 + (lane >> 3), p.N - 1);
-    boff[u] = (uint32_t)n * (uint32_t)p.ldb + dchunk;
+    const int rl = wave * (BN / 4) + u * 8 + (lane >> 3);
+    const int n = min(n0 + rl, p.N - 1);
+    boff[u] = ((uint32_t)n * (uint32_t)p.ldb + (uint32_t)(((lane & 7) ^ swz_key(rl)) * EPC)) *
+              (uint32_t)sizeof(S);
   }
+  const uint32_t lds_base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)lds);
+  const uint32_t a_dst = lds_base + (uint32_t)(wave * (BM / 4)) * 128u;
+  const uint32_t b_dst = lds_base + (uint32_t)(BM + wave * (BN / 4)) * 128u;
 
-  const int ksl = p.K / BK;               // slices per group
-  const int nsl = ksl * p.kgroups;        // total slices
-
-  auto issue = [&](int s, uint4* base) {
-    const int g = s / ksl;
-    const int k0 = (s - g * ksl) * BK;
-    const S* Ag = Az + g * p.gA + k0;
-    const S* Bg = Bz + (g % p.gBmod) * p.gB + k0;
-#pragma unroll
-    for (int u = 0; u < AI; ++u) dma16(Ag + aoff[u], base + (wave * (BM / 4) + u * 8) * CH);
-#pragma unroll
-    for (int u = 0; u < BI; ++u)
-      dma16(Bg + boff[u], base + (BM + wave * (BN / 4) + u * 8) * CH);
+  // Source of the next slice to load: (K group, k offset) advanced one slice at a time.
+  const int ksl = p.K / BK;                // slices per K group
+  const int nsl = ksl * p.kgroups;         // total slices
+  const char* a_src = reinterpret_cast<const char*>(Az);
+  const char* b_src = reinterpret_cast<const char*>(Bz);
+  int ld_k = 0, ld_g = 0, ld_bg = 0;
+  auto advance_src = [&]() {
+    if (++ld_k < ksl) {
+      a_src += BK * sizeof(S);
+      b_src += BK * sizeof(S);
+    } else {
+      ld_k = 0;
+      ++ld_g;
+      if (++ld_bg == p.gBmod) ld_bg = 0;
+      a_src = reinterpret_cast<const char*>(Az + ld_g * p.gA);
+      b_src = reinterpret_cast<const char*>(Bz + ld_bg * p.gB);
+    }
+  };
+  // DMA instruction u (A rows first, then B rows) of the current source slice into the
+  // stage at byte offset `stage`.
+  auto dma_item = [&](uint32_t stage, auto U) {
+    constexpr int u = decltype(U)::value;
+    if constexpr (u < AI)
+      dma16(a_dst + stage + u * 1024u, a_src, aoff[u]);
+    else
+      dma16(b_dst + stage + (u - AI) * 1024u, b_src, boff[u - AI]);
   };
 
   f32x16 acc[FM][FN];
@@ -180,58 +230,83 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // LDS fragment addresses (uint4 index inside a stage): row-dependent part is fixed.
-  int arow[FM], brow[FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i) arow[i] = (wm * TM + i * 32 + lrow) * CH;
-#pragma unroll
-  for (int j = 0; j < FN; ++j) brow[j] = (BM + wn * TN + j * 32 + lrow) * CH;
-  const int sw = lrow & 7;   // (row & 7) is lrow & 7 for every fragment row
-
+  // Fragment reads (uint4 index inside the ring).  Row r of a tile holds its logical
+  // chunk k at physical chunk k ^ swz_key(r); for fragment row wm*TM + 32i + lrow that key
+  // is swz_key(lrow) ^ 4(i & 1) because TM and TN are multiples of 64.
+  static_assert(TM % 64 == 0 || TM == 32, "fragment swizzle identity needs TM % 64 == 0");
+  const int arow = (wm * TM + lrow) * CH, brow = (BM + wn * TN + lrow) * CH;
+  const int sw = swz_key(lrow);
   uint4 af[2][FM], bfr[2][FN];
-  auto read_frags = [&](const uint4* L, int c, int slot) {
-    const int ch = (2 * c + lhalf) ^ sw;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) af[slot][i] = L[arow[i] + ch];
-#pragma unroll
-    for (int j = 0; j < FN; ++j) bfr[slot][j] = L[brow[j] + ch];
+  // Read k of a chunk: 0 -> A block 0, 1..FN -> B blocks, then A blocks 1..FM-1, the order
+  // in which the chunk's MFMAs (i outer, j inner) first need them.
+  auto read_item = [&](int stage_idx, auto Cc, auto Slot, auto K) {
+    constexpr int c = decltype(Cc)::value, slot = decltype(Slot)::value;
+    constexpr int k = decltype(K)::value;
+    constexpr bool is_a = k == 0 || k > FN;
+    constexpr int idx = k == 0 ? 0 : (k <= FN ? k - 1 : k - FN);
+    const int ch = ((2 * c + lhalf) ^ sw) ^ ((idx & 1) * 4);
+    if constexpr (is_a)
+      af[slot][idx] = lds[stage_idx + arow + idx * 32 * CH + ch];
+    else
+      bfr[slot][idx] = lds[stage_idx + brow + idx * 32 * CH + ch];
   };
 
-  issue(0, lds);
+  // Prologue: slice 0 into stage 0, then the fragments of its first chunk.
+  static_for<0, ND>([&](auto U) { dma_item(0u, U); });
+  advance_src();
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  read_frags(lds, 0, 0);
+  static_for<0, NR>([&](auto K) { read_item(0, I<0>{}, I<0>{}, K); });
 
-  // Software pipeline: the fragments of the next 16-deep K chunk are read while the
-  // MFMAs of the current chunk run.  At the last chunk of a slice the wave first waits
-  // for its own DMA, meets the others at the barrier (after which the next slice is in
-  // LDS and nobody reads the current one any more) and reads the next slice's first
-  // chunk, all before issuing this chunk's MFMAs, so the barrier and the reload
-  // latency overlap matrix work already in flight.  The scheduling fences keep the
-  // compiler from sinking the reads next to their uses.
-  for (int s = 0; s < nsl; ++s) {
-    const bool more = s + 1 < nsl;
-    const uint4* cur_buf = lds + (s & 1) * STAGE;
-    uint4* next_buf = lds + ((s + 1) & 1) * STAGE;
-    if (more) issue(s + 1, next_buf);
-#pragma unroll
-    for (int c = 0; c < CH / 2; ++c) {
-      const int cur = c & 1;
-      if (c + 1 < CH / 2) {
-        read_frags(cur_buf, c + 1, cur ^ 1);
-      } else {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (more) read_frags(next_buf, 0, cur ^ 1);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma_chunk<S>(af[cur][i], bfr[cur][j], acc[i][j]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
+  // One slice: NCH chunks of NM MFMAs each.  The instruction order is fixed (a scheduling
+  // fence after every MFMA slot) so that every non-MFMA instruction issues in the shadow
+  // of a running MFMA:
+  //   chunk c < NCH-1: the next chunk's NR fragment reads over the first NM/2 MFMAs;
+  //   chunks 0 and 1 (all but the last slice): the ND DMAs of slice s+1 into the other
+  //     stage, evenly spread;
+  //   last chunk: after MFMA BAR the wave waits for its DMAs and meets the others at the
+  //     barrier (slice s+1 is then in LDS and nobody reads slice s any more), and the
+  //     reads of slice s+1's first chunk go out over the remaining MFMAs.
+  auto slice = [&](int s, auto Load) {
+    constexpr bool LOAD = decltype(Load)::value;
+    const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
+    const uint32_t nxt_bytes = (uint32_t)nxt * 16u;
+    static_for<0, NCH>([&](auto Cc) {
+      constexpr int c = decltype(Cc)::value;
+      constexpr int slot = c & 1;
+      static_for<0, NM>([&](auto T) {
+        constexpr int t = decltype(T)::value;
+        constexpr int i = t / FN, j = t % FN;
+        acc[i][j] = mfma_chunk<S>(af[slot][i], bfr[slot][j], acc[i][j]);
+        if constexpr (c + 1 < NCH) {
+          static_for<0, NR>([&](auto K) {
+            if constexpr (spread_slot(decltype(K)::value, NR, 0, NM / 2) == t)
+              read_item(cur, I<c + 1>{}, I<slot ^ 1>{}, K);
+          });
+        }
+        if constexpr (LOAD && c < DCH) {
+          static_for<0, ND>([&](auto U) {
+            if constexpr (spread_slot(decltype(U)::value, ND, 0, DCH * NM) == c * NM + t)
+              dma_item(nxt_bytes, U);
+          });
+        }
+        if constexpr (LOAD && c + 1 == NCH) {
+          if constexpr (t == BAR) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+          }
+          static_for<0, NR>([&](auto K) {
+            if constexpr (spread_slot(decltype(K)::value, NR, BAR, NM) == t)
+              read_item(nxt, I<0>{}, I<slot ^ 1>{}, K);
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
+    if constexpr (LOAD) advance_src();
+  };
+  for (int s = 0; s + 1 < nsl; ++s) slice(s, std::true_type{});
+  slice(nsl - 1, std::false_type{});
   __syncthreads();
 
   // ---- epilogue.  Each wave stages one 32-row block of its tile at a time through its
