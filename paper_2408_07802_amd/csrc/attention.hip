@@ -6,8 +6,8 @@
 // each half); vt [n][d][ldv] holds V transposed (feature-major), written that
 // way by the V projection so that V^T tiles are contiguous rows.
 //
-// Formulation: a wave owns 64 queries (two 32-query MFMA blocks) and computes
-// the score tile transposed, S^T = K Q^T.  In the MFMA result layout a lane
+// Formulation: a wave owns one or two 32-query MFMA blocks and computes the
+// score tile transposed, S^T = K Q^T.  In the MFMA result layout a lane
 // then owns one query (one column) and half of the keys, so the running max /
 // sum of the online softmax are per-lane values; only the max is exchanged
 // once per tile with the partner lane (lane ^ 32).  The output is accumulated
@@ -20,9 +20,11 @@
 // keys a lane feeds to one P V MFMA are contiguous and the V^T operand is a
 // single 16-byte LDS read.
 //
-// Workgroup: 4 waves = 256 queries of one (sub-layer, head, sequence).  K and
-// V^T tiles of 64 keys are copied from HBM straight into a 3-stage LDS ring
-// (global_load_lds_dwordx4), two tiles ahead of the tile being computed.
+// Workgroup: 256 queries of one (sub-layer, head, sequence), as 8 waves of 32
+// queries (two waves per SIMD, so one wave's softmax arithmetic runs while the
+// other's MFMAs do) or, for tiles that do not split over 8 waves, 4 waves of 64.
+// K and V^T tiles of 64 keys are copied from HBM straight into a 3-stage LDS
+// ring (global_load_lds_dwordx4), two tiles ahead of the tile being computed.
 // Workgroups are ordered heaviest (longest causal prefix) first.
 #include "kraken_internal.hpp"
 #include "../../include/kraken.h"
@@ -30,10 +32,8 @@
 namespace kraken {
 namespace {
 
-constexpr int QW = 64;               // queries per wave
-constexpr int BQ = 4 * QW;           // queries per workgroup
+constexpr int BQ = 256;              // queries per workgroup
 constexpr int BKV = 64;              // keys per tile
-constexpr int ATT_THREADS = 256;
 
 struct AttnParams {
   const void* qk;
@@ -59,8 +59,17 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 __device__ __forceinline__ int kperm(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
-// 16-byte-chunk swizzle of K rows: distinct for the 8 rows one 8-lane group reads.
-__device__ __forceinline__ int ksw(int row) { return (row & 3) | ((row >> 1) & 4); }
+// Chunk swizzle of a tile with NC 16-byte chunks per row: logical chunk c of row r sits at
+// physical chunk c ^ row_key<NC>(r).  One ds_read_b128 serves 16 lanes per LDS cycle; the
+// fragment reads here give those 16 lanes 16 distinct rows (of one aligned block of 16)
+// and the same logical chunk, and the key makes their 16 (bank-group) positions
+// (r * NC + physical chunk) mod 16 distinct, so the reads are free of bank conflicts.
+template <int NC>
+__device__ __forceinline__ int row_key(int r) {
+  if constexpr (NC >= 16) return r & 15;
+  else if constexpr (NC == 8) return (r >> 1) & 7;
+  else return (r >> 2) & 3;
+}
 
 template <typename S>
 __device__ __forceinline__ void store_out4(S* dst, float a, float b, float c, float e);
@@ -92,22 +101,26 @@ __device__ __forceinline__ void wait_vmcnt() {
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-template <typename S, int HD>
-__global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
+// NQB 32-query blocks per wave: NQB = 1 runs 8 waves (two per SIMD, so one wave's
+// softmax arithmetic overlaps the other's matrix work); NQB = 2 runs 4 waves.
+template <typename S, int HD, int NQB>
+__global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams p) {
+  constexpr int QW = 32 * NQB;                // queries per wave
+  constexpr int NW = BQ / QW;                 // waves per workgroup
   constexpr int ES = sizeof(S);
   constexpr int EPC = 16 / ES;                // elements per 16-byte chunk
   constexpr int CHK = HD * ES / 16;           // chunks per K row
-  constexpr int KSWM = (CHK < 8 ? CHK : 8) - 1;
   constexpr int VCH = BKV * ES / 16;          // chunks per V^T row
   constexpr int NQC = HD * ES / 32;           // chunk pairs per head row (MFMA k steps)
   constexpr int OB = HD / 32;                 // 32-row blocks of O^T
   constexpr int TILE = BKV * HD * ES;         // bytes of one K (or V^T) tile
   constexpr int STAGE = 2 * TILE;
   constexpr int STAGES = 3 * STAGE <= 144 * 1024 ? 3 : 2;
-  constexpr int KI = CHK / 4;                 // K DMA instructions per wave per tile
-  constexpr int VI = HD * VCH / 256;          // V^T DMA instructions per wave per tile
+  constexpr int KI = CHK / NW;                // K DMA instructions per wave per tile
+  constexpr int VI = HD * VCH / 64 / NW;      // V^T DMA instructions per wave per tile
   constexpr int NPT = KI + VI;                // DMA instructions per wave per tile
-  static_assert(KI >= 1 && VI >= 1, "tile too small for the workgroup");
+  static_assert(KI >= 1 && VI >= 1 && KI * NW == CHK && VI * NW * 64 == HD * VCH,
+                "tile does not split evenly over the waves");
 
   __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
 
@@ -138,9 +151,9 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
   const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.d + h * HD) * p.ldv;
 
   // ---- Q fragments (B operand of S^T = K Q^T): lane's query, chunk 2*kc + lhalf
-  uint4 qf[2][NQC];
+  uint4 qf[NQB][NQC];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     const int q = wq0 + qb * 32 + lrow;
     const S* qrow = qkz + (int64_t)min(q, p.T - 1) * ld_qk + h * HD;
 #pragma unroll
@@ -158,7 +171,7 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
       const int ins = wave * KI + u;                       // 1 KB = 64 / CHK rows
       const int row = ins * (64 / CHK) + lane / CHK;
       const int pch = lane % CHK;
-      const int lch = pch ^ (ksw(row) & KSWM);
+      const int lch = pch ^ row_key<CHK>(row);
       const int key = min(kt0 + row, p.T - 1);
       dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
     }
@@ -167,20 +180,25 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
       const int ins = wave * VI + u;                       // 1 KB = 64 / VCH rows
       const int row = ins * (64 / VCH) + lane / VCH;
       const int pch = lane % VCH;
-      const int lch = pch ^ (row & 7);
+      const int lch = pch ^ row_key<VCH>(row);
       const int key = min(kt0 + lch * EPC, p.ldv - EPC);
       dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
     }
   };
 
-  f32x16 oacc[2][OB];
+  f32x16 oacc[NQB][OB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
+  for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
     for (int ob = 0; ob < OB; ++ob)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[qb][ob][r] = 0.f;
-  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
+  float m_run[NQB], l_run[NQB];
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    m_run[qb] = -1e30f;
+    l_run[qb] = 0.f;
+  }
 
   const int n_tiles = (q_hi - kv_begin + BKV - 1) / BKV;
 #pragma unroll
@@ -205,31 +223,29 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
     if (wq0 >= q_hi || kt0 > min(wq0 + QW - 1, q_hi - 1)) continue;
 
     // S^T for keys [kt0, kt0 + 64): two 32-key blocks per query block
-    f32x16 st[2][2];
+    f32x16 st[NQB][2];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[qb][sb][r] = 0.f;
+    // (k steps outer, key blocks inner: consecutive MFMAs feed independent accumulators)
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const int row = kperm(sb * 32 + lrow);
+    for (int kc = 0; kc < NQC; ++kc)
 #pragma unroll
-      for (int kc = 0; kc < NQC; ++kc) {
-        const uint4 a = Ks[row * CHK + ((2 * kc + lhalf) ^ (ksw(row) & KSWM))];
-        st[0][sb] = mfma_chunk<S>(a, qf[0][kc], st[0][sb]);
-        st[1][sb] = mfma_chunk<S>(a, qf[1][kc], st[1][sb]);
+      for (int sb = 0; sb < 2; ++sb) {
+        const int row = kperm(sb * 32 + lrow);
+        const uint4 a = Ks[row * CHK + ((2 * kc + lhalf) ^ row_key<CHK>(row))];
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) st[qb][sb] = mfma_chunk<S>(a, qf[qb][kc], st[qb][sb]);
       }
-    }
 
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < NQB; ++qb) {
       const int my_q = wq0 + qb * 32 + lrow;
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) st[qb][sb][r] *= p.scale_log2;
+      // scores stay unscaled here; the scale (positive) enters the running max and, fused,
+      // the exponent argument
       if ((kt0 < seq_start) || (kt0 + BKV - 1 > wq0 + qb * 32)) {
         // keys outside [seq_start, my_q] get weight 0; register r holds key
         // kt0 + 8 lhalf + off(r) with off(r) = 32 sb + 16 (r / 8) + r % 8, so the test is
@@ -245,11 +261,12 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
             st[qb][sb][r] = (off - lo <= span) ? st[qb][sb][r] : -INFINITY;
           }
       }
-      float mx = m_run[qb];
+      float mraw = -INFINITY;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[qb][sb][r]);
+        for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, st[qb][sb][r]);
+      float mx = fmaxf(m_run[qb], mraw * p.scale_log2);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       // The exponent base m_run is only moved when some lane's maximum exceeds it by
       // more than 8 (log2 units): weights stay <= 2^8, exact in the fp32 sums and within
@@ -268,7 +285,7 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(st[qb][sb][r] - m_run[qb]);
+          const float e = __builtin_amdgcn_exp2f(fmaf(st[qb][sb][r], p.scale_log2, -m_run[qb]));
           st[qb][sb][r] = e;
           lsum += e;
         }
@@ -278,9 +295,9 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
     // O^T += V^T P^T
     if constexpr (ES == 2) {
       typedef S s8 __attribute__((ext_vector_type(8)));
-      uint4 pb[2][2][2];
+      uint4 pb[NQB][2][2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -290,19 +307,20 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
             for (int j = 0; j < 8; ++j) v[j] = (S)st[qb][sb][8 * hh + j];
             pb[qb][sb][hh] = __builtin_bit_cast(uint4, v);
           }
+      // (key chunks outer, output blocks inner: independent accumulators back to back)
 #pragma unroll
-      for (int ob = 0; ob < OB; ++ob) {
-        const int m = ob * 32 + lrow;
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
+          for (int ob = 0; ob < OB; ++ob) {
+            const int m = ob * 32 + lrow;
             // k = 8 lhalf + j  <->  key 32 sb + 16 hh + 8 lhalf + j: one 16-byte chunk
-            const uint4 a = Vs[m * VCH + ((4 * sb + 2 * hh + lhalf) ^ (m & 7))];
-            oacc[0][ob] = mfma_chunk<S>(a, pb[0][sb][hh], oacc[0][ob]);
-            oacc[1][ob] = mfma_chunk<S>(a, pb[1][sb][hh], oacc[1][ob]);
+            const uint4 a = Vs[m * VCH + ((4 * sb + 2 * hh + lhalf) ^ row_key<VCH>(m))];
+#pragma unroll
+            for (int qb = 0; qb < NQB; ++qb)
+              oacc[qb][ob] = mfma_chunk<S>(a, pb[qb][sb][hh], oacc[qb][ob]);
           }
-      }
     } else {
 #pragma unroll
       for (int ob = 0; ob < OB; ++ob) {
@@ -313,14 +331,13 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
           for (int g = 0; g < 4; ++g) {
             // registers 4g .. 4g+3 hold keys 32 sb + 16 (g/2) + 8 lhalf + 4 (g%2) + (0..3)
             const int c = 8 * sb + 4 * (g >> 1) + 2 * lhalf + (g & 1);
-            const f32x4 a4 = __builtin_bit_cast(f32x4, Vs[m * VCH + (c ^ (m & 7))]);
+            const f32x4 a4 = __builtin_bit_cast(f32x4, Vs[m * VCH + (c ^ row_key<VCH>(m))]);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              oacc[0][ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[0][sb][4 * g + q],
-                                                                 oacc[0][ob], 0, 0, 0);
-              oacc[1][ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[1][sb][4 * g + q],
-                                                                 oacc[1][ob], 0, 0, 0);
-            }
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int qb = 0; qb < NQB; ++qb)
+                oacc[qb][ob] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[q], st[qb][sb][4 * g + q],
+                                                                    oacc[qb][ob], 0, 0, 0);
           }
       }
     }
@@ -328,7 +345,7 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
 
   // ---- normalise and write O (lane: query, features ob*32 + (r/4)*8 + 4*lhalf + r%4)
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
     const int my_q = wq0 + qb * 32 + lrow;
     if (my_q < q_hi) {
@@ -346,14 +363,27 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attn_kernel(AttnParams p) {
   }
 }
 
+// 8 waves of one query block each when the K and V^T tiles split evenly over 8 waves
+// (all head sizes but 32 with 16-bit storage), else 4 waves of two.
+template <typename S, int HD>
+constexpr int nqb_for() {
+  return ((HD * (int)sizeof(S) / 16) % 8 == 0) ? 1 : 2;
+}
+
+template <typename S, int HD>
+void launch_hd(const AttnParams& p, dim3 grid, hipStream_t s) {
+  constexpr int NQB = nqb_for<S, HD>();
+  hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
+}
+
 template <typename S>
 hipError_t launch_typed(const AttnParams& p, int n, int hd, hipStream_t s) {
   const int total_tiles = p.tile_prefix[p.num_seqs];
-  dim3 grid((unsigned)(n * p.n_heads), (unsigned)total_tiles), block(ATT_THREADS);
+  dim3 grid((unsigned)(n * p.n_heads), (unsigned)total_tiles);
   switch (hd) {
-    case 32: hipLaunchKernelGGL((attn_kernel<S, 32>), grid, block, 0, s, p); break;
-    case 64: hipLaunchKernelGGL((attn_kernel<S, 64>), grid, block, 0, s, p); break;
-    case 128: hipLaunchKernelGGL((attn_kernel<S, 128>), grid, block, 0, s, p); break;
+    case 32: launch_hd<S, 32>(p, grid, s); break;
+    case 64: launch_hd<S, 64>(p, grid, s); break;
+    case 128: launch_hd<S, 128>(p, grid, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
