@@ -312,9 +312,14 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   // ---- epilogue.  Each wave stages one 32-row block of its tile at a time through its
   // own quarter of the (now idle) LDS ring: the MFMA layout (lane = column, 16 rows per
   // lane) is written out as fp32 rows, then read back four consecutive columns per lane
-  // so that global stores (and residual loads) are 16-byte-per-lane row segments.
+  // so that global stores (and residual loads) are 16-byte-per-lane row segments.  The
+  // residual segments go through a two-deep register ring of half blocks: the loads of
+  // half block g + 2 are issued as soon as half block g is stored, so their latency
+  // overlaps the following stores and staging.  The row bias of the transposed
+  // projection is added after the read-back, once per 4-column segment.
   using OutT = typename std::conditional<EPI == EPI_BIAS_N_RES, float, S>::type;
   constexpr int RS = TN + 4;                           // staged row stride (floats)
+  constexpr int QN = 32 * TN / 256;                    // 4-column segments per lane per block
   static_assert(32 * RS * 4 * 4 <= (int)sizeof(lds), "epilogue staging exceeds LDS");
   float* stage = reinterpret_cast<float*>(lds) + wave * 32 * RS;
   const float* biasz = p.bias ? p.bias + z * p.sBias : nullptr;
@@ -322,6 +327,25 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   OutT* Cz = static_cast<OutT*>(p.C) + z * p.sC;
   const bool vec_ok = (p.ldc & 3) == 0;
   const int rows0 = m0 + wm * TM, cols0 = n0 + wn * TN;
+  // segment q of block i: row ml, columns nl .. nl + 3 of the wave's sub-tile
+  auto seg_ml = [&](int q) { return (q * 64 + lane) / (TN / 4); };
+  auto seg_nl = [&](int q) { return ((q * 64 + lane) % (TN / 4)) * 4; };
+  constexpr int QH = QN / 2;                           // segments per half block
+  float4 rbuf[2][QH];
+  auto load_res = [&](int g, float4* dst) {            // half block g = 2 i + h
+#pragma unroll
+    for (int qq = 0; qq < QH; ++qq) {
+      const int q = (g & 1) * QH + qq;
+      const int m = rows0 + (g >> 1) * 32 + seg_ml(q), n = cols0 + seg_nl(q);
+      dst[qq] = (Rz && vec_ok && m < p.M && n + 3 < p.N)
+                    ? *reinterpret_cast<const float4*>(Rz + (int64_t)m * p.ldc + n)
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  if constexpr (EPI == EPI_BIAS_N_RES) {
+    load_res(0, rbuf[0]);
+    load_res(1, rbuf[1]);
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -333,13 +357,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ml = (r >> 2) * 8 + lhalf * 4 + (r & 3);
-        float v = acc[i][j][r];
-        if constexpr (EPI == EPI_BIAS_M) {
-          const int m = rows0 + i * 32 + ml;
-          v += (biasz && m < p.M) ? biasz[m] : 0.f;
-        } else {
-          v += bn;
-        }
+        float v = acc[i][j][r] + bn;
         if constexpr (EPI == EPI_BIAS_N_GELU) v = gelu_erf(v);
         stage[ml * RS + nl] = v;
       }
@@ -347,19 +365,24 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
     __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int q = 0; q < 32 * TN / 256; ++q) {
-      const int e = q * 64 + lane;                     // float4 index inside the block
-      const int ml = e / (TN / 4), nl = (e % (TN / 4)) * 4;
+    for (int q = 0; q < QN; ++q) {
+      if constexpr (EPI == EPI_BIAS_N_RES) {
+        // half block 2i + h - 1 is fully stored: refill its ring slot two halves ahead
+        if (q == QH && 2 * i + 2 < 2 * FM) load_res(2 * i + 2, rbuf[0]);
+      }
+      const int ml = seg_ml(q), nl = seg_nl(q);
       const int m = rows0 + i * 32 + ml, n = cols0 + nl;
       if (m >= p.M) continue;
       float4 v = *reinterpret_cast<const float4*>(stage + ml * RS + nl);
+      if constexpr (EPI == EPI_BIAS_M) {
+        const float bm = biasz ? biasz[m] : 0.f;
+        v.x += bm; v.y += bm; v.z += bm; v.w += bm;
+      }
       OutT* dst = Cz + (int64_t)m * p.ldc + n;
       if (vec_ok && n + 3 < p.N) {
         if constexpr (EPI == EPI_BIAS_N_RES) {
-          if (Rz) {
-            const float4 rr = *reinterpret_cast<const float4*>(Rz + (int64_t)m * p.ldc + n);
-            v.x += rr.x; v.y += rr.y; v.z += rr.z; v.w += rr.w;
-          }
+          const float4 rr = rbuf[q / QH][q % QH];
+          v.x += rr.x; v.y += rr.y; v.z += rr.z; v.w += rr.w;
         }
         store4<OutT>(dst, v);
       } else {
@@ -374,6 +397,9 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
           store_val<OutT>(dst + k, o);
         }
       }
+    }
+    if constexpr (EPI == EPI_BIAS_N_RES) {
+      if (2 * i + 3 < 2 * FM) load_res(2 * i + 3, rbuf[1]);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
