@@ -39,13 +39,40 @@ struct AttnParams {
   const void* qk;
   const void* vt;
   void* out;
-  int T, d, n_heads, ldv, num_seqs;
+  int n, T, d, n_heads, ldv, num_seqs;
+  int head_group;         // heads per XCD group of the workgroup order (0: plain order)
   float scale_log2;       // log2(e) / sqrt(hd)
   int cu[KRAKEN_MAX_SEQS + 1];
   int tile_prefix[KRAKEN_MAX_SEQS + 1];
 };
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// Workgroup order.  Workgroup b runs on XCD b % 8 (round-robin dispatch), and each XCD
+// has its own L2.  With head_group G > 0 (the host sets it when the (sub-layer, head)
+// pairs split evenly over the 8 XCDs and there are many rounds of workgroups), XCD k
+// takes pairs k, k + 8, ... in groups of G, and inside a group goes through the query
+// tiles heaviest first, interleaving the group's heads.  The ~32 workgroups an XCD runs
+// at a time then cover a few heads at several query tiles each; they sweep the same K/V
+// tiles at about the same time and share them in L2.  Otherwise (few rounds, where the
+// tail of a heaviest-first order matters more) the order is heaviest tile first over all
+// pairs.
+constexpr int HEAD_GROUP = 4;
+__device__ __forceinline__ void head_rank_of(int b, int pairs, int tiles, int G, int& x,
+                                             int& rank) {
+  if (G == 0) {
+    x = b % pairs;
+    rank = b / pairs;
+    return;
+  }
+  const int k = b & 7, j = b >> 3;
+  const int per_xcd = pairs >> 3;
+  const int g = j / (G * tiles);
+  const int gsize = min(G, per_xcd - g * G);
+  const int r = j - g * G * tiles;
+  rank = r / gsize;
+  x = k + 8 * (g * G + r % gsize);
+}
 
 // 16 bytes per lane from global memory into LDS at `lds` + 16 * lane; ordered by the
 // kernel's own s_waitcnt vmcnt + barrier (see the GEMM for why it is inline assembly).
@@ -125,9 +152,10 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
   __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
 
   // ---- which (sub-layer, head, sequence, query tile)
-  const int i = blockIdx.x / p.n_heads;
-  const int h = blockIdx.x - i * p.n_heads;
-  const int rank = blockIdx.y;
+  int x, rank;
+  head_rank_of(blockIdx.x, p.n * p.n_heads, p.tile_prefix[p.num_seqs], p.head_group, x, rank);
+  const int i = x / p.n_heads;
+  const int h = x - i * p.n_heads;
   int lo = 0, hi = p.num_seqs - 1;           // last b with tile_prefix[b] <= rank
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -379,7 +407,7 @@ void launch_hd(const AttnParams& p, dim3 grid, hipStream_t s) {
 template <typename S>
 hipError_t launch_typed(const AttnParams& p, int n, int hd, hipStream_t s) {
   const int total_tiles = p.tile_prefix[p.num_seqs];
-  dim3 grid((unsigned)(n * p.n_heads), (unsigned)total_tiles);
+  dim3 grid((unsigned)(n * p.n_heads * total_tiles));
   switch (hd) {
     case 32: launch_hd<S, 32>(p, grid, s); break;
     case 64: launch_hd<S, 64>(p, grid, s); break;
@@ -395,7 +423,7 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s) {
   if (a.num_seqs <= 0 || a.num_seqs > KRAKEN_MAX_SEQS || a.n <= 0) return hipErrorInvalidValue;
   AttnParams p;
   p.qk = a.qk; p.vt = a.vt; p.out = a.out;
-  p.T = a.T; p.d = a.d; p.n_heads = a.n_heads; p.ldv = vt_ld(a.T); p.num_seqs = a.num_seqs;
+  p.n = a.n; p.T = a.T; p.d = a.d; p.n_heads = a.n_heads; p.ldv = vt_ld(a.T); p.num_seqs = a.num_seqs;
   const int hd = a.d / a.n_heads;
   p.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
   p.tile_prefix[0] = 0;
@@ -403,6 +431,8 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s) {
   for (int b = 0; b < a.num_seqs; ++b)
     p.tile_prefix[b + 1] = p.tile_prefix[b] + (a.cu_host[b + 1] - a.cu_host[b] + BQ - 1) / BQ;
   if (p.tile_prefix[a.num_seqs] == 0) return hipSuccess;
+  const int64_t pairs = (int64_t)a.n * a.n_heads, wgs = pairs * p.tile_prefix[a.num_seqs];
+  p.head_group = (pairs % 8 == 0 && wgs >= 2048) ? HEAD_GROUP : 0;
   switch (a.dt) {
     case DType::BF16: return launch_typed<bf16>(p, a.n, hd, s);
     case DType::F16: return launch_typed<f16>(p, a.n, hd, s);
