@@ -30,9 +30,18 @@ COMMON_FLAGS = [
 ]
 
 
+# Per-file additions.  Attention: for finite inputs its softmax only takes maxima of finite
+# scores and -inf; without IEEE mode the compiler drops the NaN-quieting instruction it
+# otherwise puts in front of every maximum.
+FILE_FLAGS = {
+    "attention.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *COMMON_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *COMMON_FLAGS, *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}\n{res.stderr}")

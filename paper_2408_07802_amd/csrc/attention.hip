@@ -26,6 +26,8 @@
 // K and V^T tiles of 64 keys are copied from HBM straight into a 3-stage LDS
 // ring (global_load_lds_dwordx4), two tiles ahead of the tile being computed.
 // Workgroups are ordered heaviest (longest causal prefix) first.
+#include <type_traits>
+
 #include "kraken_internal.hpp"
 #include "../../include/kraken.h"
 
@@ -391,6 +393,349 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Ping-pong form for 16-bit operands: 8 waves of 32 queries, two waves per SIMD.  Each
+// wave alternates a matrix phase M(t) = { O^T += V(t-1)^T P(t-1)^T, S(t) = K(t) Q^T } and a
+// vector phase V(t) = { online softmax of S(t): mask, running max, exponentials, row sums,
+// 16-bit P(t) }, with a workgroup barrier after every phase.  One group of four waves starts
+// one barrier later than the other, so the two waves sharing a SIMD are in opposite phases
+// and one wave's softmax arithmetic runs while the other's MFMAs do.  K/V^T tiles go
+// through a 4-stage LDS ring.  Numbering the intervals between barriers (interval k ends
+// at barrier k), the leading group runs M(t) in interval 2t+1 and V(t) in 2t+2, the
+// trailing group one interval later; so K(u) is read in intervals 2u+1 and 2u+2, V(u) in
+// 2u+3 and 2u+4.  Every wave issues its share of tile u in interval 2u-3 (leading group
+// in M(u-2), trailing group in V(u-3)), when tile u-4, the stage's previous tile, is no
+// longer read, and waits for that share just before barrier 2u (leading group in V(u-1),
+// trailing group in M(u-1)), so the tile is complete before its first reader.
+constexpr int PP_STAGES = 4;
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int N>
+using IC = std::integral_constant<int, N>;
+
+template <int B, int E, typename F>
+__device__ __forceinline__ void sfor(F&& f) {
+  if constexpr (B < E) {
+    f(IC<B>{});
+    sfor<B + 1, E>(f);
+  }
+}
+
+// Sum of the eight 16-bit values packed in v, added to acc in fp32 (v_dot2 with (1, 1)).
+template <typename S>
+__device__ __forceinline__ float sum8(uint4 v, float acc);
+template <>
+__device__ __forceinline__ float sum8<f16>(uint4 v, float acc) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const h2 one = {(_Float16)1.0f, (_Float16)1.0f};
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, v.x), one, acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, v.y), one, acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, v.z), one, acc, false);
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, v.w), one, acc, false);
+}
+template <>
+__device__ __forceinline__ float sum8<bf16>(uint4 v, float acc) {
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  const b2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, v.x), one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, v.y), one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, v.z), one, acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, v.w), one, acc, false);
+}
+
+template <typename S, int HD>
+__global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
+  constexpr int NW = 8, QW = 32;
+  constexpr int EPC = 8;                      // 16-bit elements per 16-byte chunk
+  constexpr int CHK = HD * 2 / 16;            // chunks per K row
+  constexpr int VCH = BKV * 2 / 16;           // chunks per V^T row
+  constexpr int NQC = HD * 2 / 32;            // 16-deep k steps of S
+  constexpr int OB = HD / 32;                 // 32-row blocks of O^T
+  constexpr int TILE = BKV * HD * 2;
+  constexpr int STAGE = 2 * TILE;
+  constexpr int KI = CHK / NW;
+  constexpr int VI = HD * VCH / 64 / NW;
+  constexpr int NPT = KI + VI;                // DMA instructions per wave per tile
+  constexpr int NS = 2 * NQC;                 // S MFMAs per tile
+  constexpr int NP = 4 * OB;                  // PV MFMAs per tile
+  constexpr int RING = 2;                     // fragment register ring depth
+  static_assert(KI >= 1 && VI >= 1 && KI * NW == CHK && VI * NW * 64 == HD * VCH,
+                "tile does not split evenly over the waves");
+  static_assert(PP_STAGES * STAGE <= 160 * 1024, "LDS ring too large");
+  static_assert(NS == NP && NS >= RING, "S and PV MFMAs alternate one for one");
+
+  __shared__ __attribute__((aligned(16))) uint4 smem[PP_STAGES * STAGE / 16];
+
+  int x, rank;
+  head_rank_of(blockIdx.x, p.n * p.n_heads, p.tile_prefix[p.num_seqs], p.head_group, x, rank);
+  const int i = x / p.n_heads;
+  const int h = x - i * p.n_heads;
+  int lo = 0, hi = p.num_seqs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.tile_prefix[mid] <= rank) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  const int ntiles_b = p.tile_prefix[b + 1] - p.tile_prefix[b];
+  const int qt = ntiles_b - 1 - (rank - p.tile_prefix[b]);
+  const int seq_start = p.cu[b], seq_end = p.cu[b + 1];
+  const int q0 = seq_start + qt * BQ;
+  const int q_hi = min(q0 + BQ, seq_end);
+  const int kv_begin = seq_start & ~7;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // group B (one barrier behind group A): waves 1, 3, 4, 6.  Whether the hardware puts waves
+  // w and w + 4 or waves 2k and 2k + 1 on one SIMD, each SIMD gets one wave of each group.
+  const bool trail = ((wave & 1) ^ (wave >> 2)) != 0;
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  const int wq0 = q0 + wave * QW;
+  const int my_q = wq0 + lrow;
+  // last key tile this wave's queries see (-1: the wave has no queries)
+  const int wlast = (wq0 >= q_hi) ? -1 : (min(wq0 + QW - 1, q_hi - 1) - kv_begin) / BKV;
+  const int n_tiles = (q_hi - kv_begin + BKV - 1) / BKV;
+
+  const int64_t ld_qk = 2 * (int64_t)p.d;
+  const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
+  const S* Kbase = qkz + p.d + h * HD;
+  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.d + h * HD) * p.ldv;
+
+  uint4 qf[NQC];
+  {
+    const S* qrow = qkz + (int64_t)min(my_q, p.T - 1) * ld_qk + h * HD;
+#pragma unroll
+    for (int kc = 0; kc < NQC; ++kc)
+      qf[kc] = (my_q < q_hi) ? *reinterpret_cast<const uint4*>(qrow + (2 * kc + lhalf) * EPC)
+                             : make_uint4(0, 0, 0, 0);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES
+  auto issue = [&](int u) {
+    if (u >= n_tiles) return;
+    const int kt0 = kv_begin + u * BKV;
+    unsigned char* base = reinterpret_cast<unsigned char*>(smem) + (u % PP_STAGES) * STAGE;
+#pragma unroll
+    for (int k = 0; k < KI; ++k) {
+      const int ins = wave * KI + k;
+      const int row = ins * (64 / CHK) + lane / CHK;
+      const int lch = (lane % CHK) ^ row_key<CHK>(row);
+      const int key = min(kt0 + row, p.T - 1);
+      dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
+    }
+#pragma unroll
+    for (int k = 0; k < VI; ++k) {
+      const int ins = wave * VI + k;
+      const int row = ins * (64 / VCH) + lane / VCH;
+      const int lch = (lane % VCH) ^ row_key<VCH>(row);
+      const int key = min(kt0 + lch * EPC, p.ldv - EPC);
+      dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
+    }
+  };
+  // this wave's share of tile u is complete (u + 1 may still be in flight)
+  auto wait_tile = [&](int u) {
+    if (u + 1 < n_tiles) wait_vm<NPT>();
+    else wait_vm<0>();
+  };
+
+  // Fragment addresses.  A fragment's physical chunk is (logical chunk) ^ key(row); the
+  // lane's own bits (lhalf and the key) are folded into a per-lane base once, so a read is
+  // (base + stage offset, a multiple of the row size) XOR a compile-time chunk offset,
+  // plus a compile-time row-block offset.
+  const uint32_t smem_base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)smem);
+  uint32_t kbase[2];
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb) {
+    const int row = kperm(sb * 32 + lrow);
+    kbase[sb] = smem_base + (uint32_t)(row * CHK * 16 + ((lhalf ^ row_key<CHK>(row)) * 16));
+  }
+  // (ob * 32 + lrow) has the same key for every ob
+  const uint32_t vbase =
+      smem_base + TILE + (uint32_t)(lrow * VCH * 16 + ((lhalf ^ row_key<VCH>(lrow)) * 16));
+  // 16-byte LDS read at byte address addr + 16 idx (typed indexing keeps the 16-byte
+  // alignment visible to the compiler, so every read is one ds_read_b128)
+  auto lds16 = [](uint32_t addr, int idx = 0) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_assume((addr & 15u) == 0);
+    const __attribute__((address_space(3))) u32x4* ptr =
+        reinterpret_cast<const __attribute__((address_space(3))) u32x4*>((size_t)addr);
+    return __builtin_bit_cast(uint4, ptr[idx]);
+  };
+  auto stage_off = [](int u) { return (uint32_t)((u % PP_STAGES) * STAGE); };
+  // operand of S MFMA j (k step j/2, key block j%2) of the tile at stage offset st
+  auto k_frag = [&](uint32_t st, int j) {
+    const int kc = j >> 1, sb = j & 1;
+    return lds16((kbase[sb] + st) ^ (uint32_t)(2 * kc * 16));
+  };
+  // operand of PV MFMA j = (key block sb, half hh, output block ob)
+  auto v_frag = [&](uint32_t st, int j) {
+    const int sb = j / (2 * OB), hh = (j / OB) & 1, ob = j % OB;
+    return lds16((vbase + st) ^ (uint32_t)((4 * sb + 2 * hh) * 16), ob * 32 * VCH);
+  };
+
+  f32x16 oacc[OB];
+#pragma unroll
+  for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[ob][r] = 0.f;
+  float m_run = -1e30f, l_run = 0.f;
+  const float scale = p.scale_log2;
+  f32x16 sacc[2];                             // S(t), key blocks 0 and 1
+  uint4 pb[2][2];                             // 16-bit P(t-1): [key block][half]
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) pb[sb][hh] = make_uint4(0, 0, 0, 0);
+  const f32x16 zero16 = {};
+
+  // M(t): PV(t-1) and S(t), alternating.  At t = 0 P is zero and V is read from tile 0's
+  // stage (real data), so the PV MFMAs add exactly zero; for t > wlast the scores are never
+  // used.  The wave's last step only needs PV.
+  auto mphase = [&](int t) {
+    const uint32_t kst = stage_off(t);
+    const uint32_t vst = stage_off(t >= 1 ? t - 1 : 0);
+    uint4 kf[RING], vf[RING];
+    sfor<0, RING>([&](auto J) {
+      kf[J()] = k_frag(kst, J());
+      vf[J()] = v_frag(vst, J());
+    });
+    sfor<0, 2 * NS>([&](auto Sl) {
+      constexpr int sl = decltype(Sl)::value;
+      constexpr int j = sl >> 1;
+      if constexpr ((sl & 1) == 0) {
+        constexpr int sb = j / (2 * OB), hh = (j / OB) & 1, ob = j % OB;
+        oacc[ob] = mfma_chunk<S>(vf[j % RING], pb[sb][hh], oacc[ob]);
+        if constexpr (j + RING < NP) vf[j % RING] = v_frag(vst, j + RING);
+      } else {
+        sacc[j & 1] = mfma_chunk<S>(kf[j % RING], qf[j >> 1], j < 2 ? zero16 : sacc[j & 1]);
+        if constexpr (j + RING < NS) kf[j % RING] = k_frag(kst, j + RING);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  // V(t): online softmax of S(t) into P(t)
+  auto vphase = [&](int t) {
+    const int kt0 = kv_begin + t * BKV;
+    // keys outside [seq_start, my_q] get weight 0 (only tiles crossing the diagonal or the
+    // sequence start): register r of key block sb holds key kt0 + 8 lhalf + off(r)
+    if ((kt0 < seq_start) || (kt0 + BKV - 1 > wq0)) {
+      const int base = kt0 + 8 * lhalf;
+      const unsigned lo_ = (unsigned)(seq_start - base);
+      const unsigned span = (unsigned)(my_q - seq_start);
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const unsigned off = (unsigned)(sb * 32 + (r >> 3) * 16 + (r & 7));
+          sacc[sb][r] = (off - lo_ <= span) ? sacc[sb][r] : -INFINITY;
+        }
+    }
+    float mraw = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[sb][r]);
+    float mx = fmaxf(m_run, mraw * scale);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                     false, false);
+    mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    // the exponent base moves only when a maximum outgrows it by more than 8 (log2):
+    // weights stay <= 2^8 and rescales of O are rare
+    if (__ballot(mx > m_run + 8.0f)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
+      l_run *= alpha;
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[ob][r] *= alpha;
+      m_run = mx;
+    }
+    // weights, packed to 16 bits for the PV MFMAs; the row sum adds the packed (rounded)
+    // weights, i.e. exactly the ones the MFMAs multiply
+    float lsum = 0.f;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sacc[sb][r] = __builtin_amdgcn_exp2f(fmaf(sacc[sb][r], scale, -m_run));
+      typedef S s8 __attribute__((ext_vector_type(8)));
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        s8 v;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = (S)sacc[sb][8 * hh + k];
+        pb[sb][hh] = __builtin_bit_cast(uint4, v);
+        lsum = sum8<S>(pb[sb][hh], lsum);
+      }
+    }
+    l_run += lsum;
+  };
+
+  // ---- prologue: group A loads tiles 0, 1, group B tiles 0, 1, 2 (their later loads are
+  // issued in M(t) and V(t)); tile 0 complete at barrier 0
+  issue(0);
+  issue(1);
+  if (trail) {
+    issue(2);
+    if (n_tiles > 2) wait_vm<2 * NPT>();
+    else if (n_tiles > 1) wait_vm<NPT>();
+    else wait_vm<0>();
+  } else {
+    if (n_tiles > 1) wait_vm<NPT>();
+    else wait_vm<0>();
+  }
+  __syncthreads();
+  if (trail) __syncthreads();                 // group B: one interval behind
+
+  for (int t = 0; t < n_tiles; ++t) {
+    // ---- M(t)
+    if (t <= wlast + 1) mphase(t);
+    if (!trail) {
+      issue(t + 2);
+    } else {
+      wait_tile(t + 1);
+    }
+    __syncthreads();
+    // ---- V(t)
+    if (t <= wlast) vphase(t);
+    if (!trail) {
+      wait_tile(t + 1);
+    } else {
+      issue(t + 3);
+    }
+    __syncthreads();
+  }
+  // ---- M(n): the last PV
+  if (n_tiles <= wlast + 1) mphase(n_tiles);
+  __syncthreads();
+  if (!trail) __syncthreads();                // group A: matches group B's extra barrier
+
+  // ---- normalise and write O (lane: query, features ob*32 + (r/4)*8 + 4*lhalf + r%4)
+  {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run),
+                                                     __float_as_uint(l_run), false, false);
+    const float l_tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    if (my_q < q_hi) {
+      const float inv = 1.0f / l_tot;
+      S* orow = static_cast<S*>(p.out) + ((int64_t)i * p.T + my_q) * p.d + h * HD;
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = ob * 32 + g * 8 + lhalf * 4;
+          store_out4(orow + m, oacc[ob][4 * g] * inv, oacc[ob][4 * g + 1] * inv,
+                     oacc[ob][4 * g + 2] * inv, oacc[ob][4 * g + 3] * inv);
+        }
+    }
+  }
+}
+
 // 8 waves of one query block each when the K and V^T tiles split evenly over 8 waves
 // (all head sizes but 32 with 16-bit storage), else 4 waves of two.
 template <typename S, int HD>
@@ -401,7 +746,11 @@ constexpr int nqb_for() {
 template <typename S, int HD>
 void launch_hd(const AttnParams& p, dim3 grid, hipStream_t s) {
   constexpr int NQB = nqb_for<S, HD>();
-  hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
+  // (the ping-pong form needs enough MFMA work per tile to cover the softmax: head size 128)
+  if constexpr (sizeof(S) == 2 && HD == 128)
+    hipLaunchKernelGGL((attn_pp_kernel<S, HD>), grid, dim3(512), 0, s, p);
+  else
+    hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
 }
 
 template <typename S>
