@@ -9,9 +9,12 @@ timed steps), and the fp64 oracle timed on a bounded sample on the host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--compute f16|bf16] [--no-cpu-baseline]
+       python bench.py --pmc-probe      (one prefill + one 1 GiB device copy, untimed:
+                                          the command the HBM counter runs profile)
 """
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -23,6 +26,21 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 MFMA_PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}   # MI355X dense
+COPY_PROBE_BYTES = 1 << 30
+
+# HBM bytes per launch of the dominant kernel, from two rocprofv3 --pmc runs of
+# `python bench.py --pmc-probe` (FETCH_SIZE, then WRITE_SIZE), each scaled by what the
+# same counter reads for the probe's 1 GiB device copy.  Valid only for the kernel source
+# they were taken on; bench.py reports null once that file changes.
+TRAFFIC = {
+    "attention": {
+        "source": "paper_2408_07802_amd/csrc/attention.hip",
+        "source_sha256": "b7afeaa372a6105952e5cc5a1611475785ad2e301445d2b554bd77cdc3e4fc4b",
+        "read_bytes": 3489426042, "write_bytes": 268916032,
+        "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
+        "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
+    },
+}
 METRIC = "prefill tokens/s + TTFT ms (all N sub-layers, 1 MI355X); MFMA util %"
 
 
@@ -60,6 +78,20 @@ def cpu_baseline(w, T, seed=0):
             "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def traffic_of(kernel):
+    """Measured HBM traffic of `kernel` per launch: (read + write bytes, detail), or
+    (None, None) when no counter run exists for the current source of the kernel."""
+    t = TRAFFIC.get(kernel)
+    if not t:
+        return None, None
+    with open(os.path.join(ROOT, t["source"]), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != t["source_sha256"]:
+            return None, None
+    return t["read_bytes"] + t["write_bytes"], {
+        "unit": "bytes/launch", "read": t["read_bytes"], "write": t["write_bytes"],
+        "algorithmic": t["algorithmic_bytes"], "profile": t["profile"]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -68,6 +100,8 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--compute", default=None, help="MFMA operand type (default: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="one prefill and one 1 GiB device copy, untimed (for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -105,6 +139,17 @@ def main():
     X = synth.gen_hidden(w, T, 0, dev)
     out = torch.empty((T, w.d_model), dtype=torch.float32, device=dev)
     log("[bench] weights loaded; warming up")
+    if args.pmc_probe:
+        model.prefill(X, cu, out=out)
+        torch.cuda.synchronize()
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] probe done: 1 prefill, then a {COPY_PROBE_BYTES}-byte device copy")
+        model.close()
+        return
 
     for _ in range(args.warmup):
         model.prefill(X, cu, out=out)
@@ -184,7 +229,8 @@ def main():
         "algorithmic_tflop_per_step": total_flops / 1e12,
         "roofline": {"bound": "mfma", "kernel": dominant,
                      "achieved": dk["tflops"], "peak": peak, "unit": "TFLOP/s",
-                     "frac": dk["tflops"] / peak, "traffic": None,
+                     "frac": dk["tflops"] / peak, "traffic": traffic_of(dominant)[0],
+                     "traffic_detail": traffic_of(dominant)[1],
                      "avg_launch_ms": dk["avg_launch_ms"],
                      "launches_per_step": dk["launches_per_step"]},
         "kernels": kernels,
