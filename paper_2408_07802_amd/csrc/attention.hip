@@ -13,9 +13,10 @@
 // once per tile with the partner lane (lane ^ 32).  The output is accumulated
 // transposed, O^T = V^T P^T, whose columns are again the lane's query, so the
 // rescale by exp(m_old - m_new) is lane-local; the exponent base only moves when
-// a maximum outgrows it by more than 2^8, so rescales are rare.  P^T goes from the S^T accumulator registers straight into
-// the B operand of the second MFMA.  The K rows of each 32-row fragment are
-// read in an order that swaps bits 2 and 3 of the row index; then result
+// a maximum outgrows it by more than 2^8, so rescales are rare.  P^T goes from the
+// S^T accumulator registers straight into the B operand of the second MFMA.  The K
+// rows of each 32-row fragment are read in an order that swaps bits 2 and 3 of the
+// row index; then result
 // register r of lane half h holds key 16 (r / 8) + 8 h + r % 8, so the eight
 // keys a lane feeds to one P V MFMA are contiguous and the V^T operand is a
 // single 16-byte LDS read.
@@ -84,6 +85,22 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
                :: "s"(l), "v"(g) : "memory", "m0");
 }
 
+// The same DMA with a wave-uniform base address (SGPR pair) and a per-lane 32-bit byte
+// offset, so that per-tile address arithmetic stays on the scalar unit.
+// (The base goes through readfirstlane so that it is an SGPR pair whatever the compiler
+// concludes about its uniformity.)
+__device__ __forceinline__ void dma16_off(uint32_t lds_addr, const void* base, uint32_t off) {
+  // (readfirstlane returns a signed int: each half is taken as unsigned before widening,
+  // or a low half with bit 31 set would sign-extend over the high half)
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint64_t bu = ((uint64_t)hi << 32) | (uint64_t)lo;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(off),
+                  "s"(reinterpret_cast<const void*>(bu)) : "memory", "m0");
+}
+
 // Key row read by fragment row r: bits 2 and 3 of r swapped.
 __device__ __forceinline__ int kperm(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -118,6 +135,9 @@ template <>
 __device__ __forceinline__ void store_out4<float>(float* dst, float a, float b, float c, float e) {
   *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, e);
 }
+
+// s_waitcnt immediate for vmcnt(0) alone (expcnt and lgkmcnt at their maximum).
+constexpr int VMCNT0 = 0x0f70;
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -191,7 +211,11 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
       qf[qb][kc] = (q < q_hi) ? *reinterpret_cast<const uint4*>(qrow + (2 * kc + lhalf) * EPC)
                               : make_uint4(0, 0, 0, 0);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // The Q loads are complete before any DMA is issued.  (The compiler's own wait, which
+  // it can see, not inline assembly: an opaque wait here would leave the loads pending in
+  // its bookkeeping, and it would then wait for every outstanding vector-memory operation,
+  // the K/V prefetches included, before the first use of Q in every tile.)
+  __builtin_amdgcn_s_waitcnt(VMCNT0);
 
   // ---- DMA of one K tile and one V^T tile into stage `st`.
   auto issue = [&](int kt0, int st) {
@@ -240,7 +264,8 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
     if (STAGES == 3 && t + 1 < n_tiles) wait_vmcnt<NPT>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if (t + STAGES - 1 < n_tiles) issue(kv_begin + (t + STAGES - 1) * BKV, (t + STAGES - 1) % STAGES);
+    if (t + STAGES - 1 < n_tiles)
+      issue(kv_begin + (t + STAGES - 1) * BKV, (t + STAGES - 1) % STAGES);
 
     const int kt0 = kv_begin + t * BKV;
     const unsigned char* base = smem + (t % STAGES) * STAGE;
@@ -462,7 +487,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   constexpr int NPT = KI + VI;                // DMA instructions per wave per tile
   constexpr int NS = 2 * NQC;                 // S MFMAs per tile
   constexpr int NP = 4 * OB;                  // PV MFMAs per tile
-  constexpr int RING = 2;                     // fragment register ring depth
+  constexpr int RING = 4;                     // fragment register ring depth
   static_assert(KI >= 1 && VI >= 1 && KI * NW == CHK && VI * NW * 64 == HD * VCH,
                 "tile does not split evenly over the waves");
   static_assert(PP_STAGES * STAGE <= 160 * 1024, "LDS ring too large");
@@ -512,28 +537,60 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
       qf[kc] = (my_q < q_hi) ? *reinterpret_cast<const uint4*>(qrow + (2 * kc + lhalf) * EPC)
                              : make_uint4(0, 0, 0, 0);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(VMCNT0);        // (visible to the compiler: see attn_kernel)
 
-  // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES
+  // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES.
+  // Lane offsets within a tile are computed once; a tile that ends inside the key range
+  // then costs one uniform base pointer (scalar arithmetic) per operand.  Only a tile
+  // reaching past the end of the key range clamps each lane's row.
+  const uint32_t smem_base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)smem);
+  uint32_t koff[KI], voff[VI];
+#pragma unroll
+  for (int k = 0; k < KI; ++k) {
+    const int row = (wave * KI + k) * (64 / CHK) + lane / CHK;
+    const int lch = (lane % CHK) ^ row_key<CHK>(row);
+    koff[k] = (uint32_t)((row * ld_qk + lch * EPC) * 2);
+  }
+#pragma unroll
+  for (int k = 0; k < VI; ++k) {
+    const int row = (wave * VI + k) * (64 / VCH) + lane / VCH;
+    const int lch = (lane % VCH) ^ row_key<VCH>(row);
+    voff[k] = (uint32_t)((row * (int64_t)p.ldv + lch * EPC) * 2);
+  }
   auto issue = [&](int u) {
     if (u >= n_tiles) return;
     const int kt0 = kv_begin + u * BKV;
+    const uint32_t st = smem_base + (uint32_t)((u % PP_STAGES) * STAGE);
     unsigned char* base = reinterpret_cast<unsigned char*>(smem) + (u % PP_STAGES) * STAGE;
+    if (kt0 + BKV <= p.T) {
+      const S* kb = Kbase + (int64_t)kt0 * ld_qk;
 #pragma unroll
-    for (int k = 0; k < KI; ++k) {
-      const int ins = wave * KI + k;
-      const int row = ins * (64 / CHK) + lane / CHK;
-      const int lch = (lane % CHK) ^ row_key<CHK>(row);
-      const int key = min(kt0 + row, p.T - 1);
-      dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
+      for (int k = 0; k < KI; ++k) dma16_off(st + (uint32_t)((wave * KI + k) * 1024), kb, koff[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < KI; ++k) {
+        const int ins = wave * KI + k;
+        const int row = ins * (64 / CHK) + lane / CHK;
+        const int lch = (lane % CHK) ^ row_key<CHK>(row);
+        const int key = min(kt0 + row, p.T - 1);
+        dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
+      }
     }
+    if (kt0 + BKV <= p.ldv) {
+      const S* vb = Vbase + kt0;
 #pragma unroll
-    for (int k = 0; k < VI; ++k) {
-      const int ins = wave * VI + k;
-      const int row = ins * (64 / VCH) + lane / VCH;
-      const int lch = (lane % VCH) ^ row_key<VCH>(row);
-      const int key = min(kt0 + lch * EPC, p.ldv - EPC);
-      dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
+      for (int k = 0; k < VI; ++k)
+        dma16_off(st + (uint32_t)(TILE + (wave * VI + k) * 1024), vb, voff[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < VI; ++k) {
+        const int ins = wave * VI + k;
+        const int row = ins * (64 / VCH) + lane / VCH;
+        const int lch = (lane % VCH) ^ row_key<VCH>(row);
+        const int key = min(kt0 + lch * EPC, p.ldv - EPC);
+        dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
+      }
     }
   };
   // this wave's share of tile u is complete (u + 1 may still be in flight)
@@ -546,8 +603,6 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   // lane's own bits (lhalf and the key) are folded into a per-lane base once, so a read is
   // (base + stage offset, a multiple of the row size) XOR a compile-time chunk offset,
   // plus a compile-time row-block offset.
-  const uint32_t smem_base =
-      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)smem);
   uint32_t kbase[2];
 #pragma unroll
   for (int sb = 0; sb < 2; ++sb) {
@@ -636,11 +691,17 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
           sacc[sb][r] = (off - lo_ <= span) ? sacc[sb][r] : -INFINITY;
         }
     }
-    float mraw = -INFINITY;
+    // (four independent chains of three-input maxima, not one chain of 16)
+    float mq[4];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+    for (int q = 0; q < 4; ++q) {
+      const f32x16& sq = sacc[q >> 1];
+      const int o = 8 * (q & 1);
+      mq[q] = fmaxf(sq[o], sq[o + 1]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[sb][r]);
+      for (int r = 2; r < 8; r += 2) mq[q] = fmaxf(fmaxf(mq[q], sq[o + r]), sq[o + r + 1]);
+    }
+    const float mraw = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
     float mx = fmaxf(m_run, mraw * scale);
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
                                                      false, false);
@@ -657,8 +718,8 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
       m_run = mx;
     }
     // weights, packed to 16 bits for the PV MFMAs; the row sum adds the packed (rounded)
-    // weights, i.e. exactly the ones the MFMAs multiply
-    float lsum = 0.f;
+    // weights, i.e. exactly the ones the MFMAs multiply (four independent partial sums)
+    float lsum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
@@ -671,10 +732,10 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = (S)sacc[sb][8 * hh + k];
         pb[sb][hh] = __builtin_bit_cast(uint4, v);
-        lsum = sum8<S>(pb[sb][hh], lsum);
+        lsum[2 * sb + hh] = sum8<S>(pb[sb][hh], lsum[2 * sb + hh]);
       }
     }
-    l_run += lsum;
+    l_run += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
   };
 
   // ---- prologue: group A loads tiles 0, 1, group B tiles 0, 1, 2 (their later loads are
@@ -772,7 +833,8 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s) {
   if (a.num_seqs <= 0 || a.num_seqs > KRAKEN_MAX_SEQS || a.n <= 0) return hipErrorInvalidValue;
   AttnParams p;
   p.qk = a.qk; p.vt = a.vt; p.out = a.out;
-  p.n = a.n; p.T = a.T; p.d = a.d; p.n_heads = a.n_heads; p.ldv = vt_ld(a.T); p.num_seqs = a.num_seqs;
+  p.n = a.n; p.T = a.T; p.d = a.d; p.n_heads = a.n_heads; p.ldv = vt_ld(a.T);
+  p.num_seqs = a.num_seqs;
   const int hd = a.d / a.n_heads;
   p.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
   p.tile_prefix[0] = 0;

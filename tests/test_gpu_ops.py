@@ -95,10 +95,27 @@ GEMM_SHAPES = [  # (M, N, K, batch)
 ]
 
 
+# Shapes of at least 512 256 x 256 tiles, which select the large-tile configuration of
+# 16-bit operands: ragged M and N edges, and the shortest K (one 64-element slice, so the
+# double-buffered ring runs only its prologue and last slice).
+GEMM_BIG_SHAPES = [(2000, 1100, 320, 15), (1024, 1024, 64, 32)]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("epi", [0, 1, 2, 3])
 @pytest.mark.parametrize("shape", GEMM_SHAPES)
 def test_gemm(dtype, epi, shape):
+    _check_gemm(dtype, epi, shape)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", GEMM_BIG_SHAPES)
+def test_gemm_big_tiles(dtype, epi, shape):
+    _check_gemm(dtype, epi, shape)
+
+
+def _check_gemm(dtype, epi, shape):
     M, N, Kd, batch = shape
     g = torch.Generator(device="cpu").manual_seed(M * 7 + N * 3 + Kd + batch + epi * 101)
     dt = tdt(dtype)
