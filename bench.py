@@ -35,8 +35,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "b7afeaa372a6105952e5cc5a1611475785ad2e301445d2b554bd77cdc3e4fc4b",
-        "read_bytes": 3489426042, "write_bytes": 268916032,
+        "source_sha256": "1a0cd80a98d02e09c33064c9a7128ce40a1ef4d094f44f092fea90a51a400da3",
+        "read_bytes": 3155395201, "write_bytes": 269239748,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
