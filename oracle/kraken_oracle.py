@@ -32,6 +32,15 @@ within each packed sequence only; ``y`` includes the sub-layer's own input
 Every function works in float64 on whatever values it is given; callers pass
 the exact dtype-rounded inputs and weights of the run being checked.
 
+Decode (the autoregressive phase after the prefill; Section 2.1 on the KV
+cache: the keys and values of every token are cached, and each decode step
+appends its own): a new token of a sequence runs the same layer stack on its own
+row; its attention sees the keys and values of every earlier token of its
+sequence, cached by the prefill (and earlier decode steps) per layer and
+sub-layer, plus its own.  By causality a decode step equals the last row of the
+prefill of the extended sequence; the pins in ``tests/test_oracle_pins.py``
+check exactly that.
+
 Weight layout taken by this module (a convention, not mathematics): every
 matrix multiplies as ``u @ W`` (row-major ``[in, out]``); ``Wqkv`` has
 columns ``[Q | K | V]`` and head ``h`` owns columns ``h*hd:(h+1)*hd`` of each.
@@ -101,12 +110,19 @@ def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int) -> np.nda
     return out
 
 
-def multi_head_attention(u, p: Mapping, cu_seqlens, n_heads: int) -> np.ndarray:
-    """MHA block: QKV projection, per-head causal attention, output projection."""
+def multi_head_attention(u, p: Mapping, cu_seqlens, n_heads: int,
+                         kv_out: list | None = None) -> np.ndarray:
+    """MHA block: QKV projection, per-head causal attention, output projection.
+
+    With ``kv_out`` (a list), appends this block's keys and values ``(K, V)``
+    (``[T, d]`` each, the projections the attention used).
+    """
     u = _f64(u)
     d = u.shape[1]
     qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
     Q, K, V = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    if kv_out is not None:
+        kv_out.append((K, V))
     return causal_attention(Q, K, V, cu_seqlens, n_heads) @ _f64(p["Wo"]) + _f64(p["bo"])
 
 
@@ -117,19 +133,20 @@ def feed_forward(u, p: Mapping) -> np.ndarray:
 
 
 def sub_layer_forward(x, y, p: Mapping, cu_seqlens, n_heads: int,
-                      eps: float = LN_EPS) -> np.ndarray:
+                      eps: float = LN_EPS, kv_out: list | None = None) -> np.ndarray:
     """One Kraken sub-layer (Algorithm 1) given its input ``x`` and combined ``y``.
 
-    ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.
+    ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.  ``kv_out``: see
+    ``multi_head_attention``.
     """
     x = _f64(x)
     h = x + multi_head_attention(layer_norm(x, p["ln1_g"], p["ln1_b"], eps),
-                                 p, cu_seqlens, n_heads)
+                                 p, cu_seqlens, n_heads, kv_out)
     return h + feed_forward(layer_norm(h + _f64(y), p["ln2_g"], p["ln2_b"], eps), p)
 
 
 def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mapping]],
-                   W_concat, n_heads: int, eps: float = LN_EPS):
+                   W_concat, n_heads: int, eps: float = LN_EPS, return_kv: bool = False):
     """Forward pass of a stack of Kraken layers followed by ``W_concat``.
 
     ``X`` is the shared first-layer input ``[T, d]`` (Section 3.1: one set of
@@ -143,10 +160,13 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
 
     Returns ``(out, sub_out)``: ``sub_out[i]`` is sub-layer i's output after the
     last layer (``[N, T, d]``) and ``out = [Y_1 | ... | Y_N] @ W_concat``
-    (``[T, d]``; Section 3.1, final combine).
+    (``[T, d]``; Section 3.1, final combine).  With ``return_kv``, also the key
+    and value projections of every layer and sub-layer, ``kv[j][i] = (K, V)``
+    (``[T, d]`` each): what a decode step attends to.
     """
     X = _f64(X)
     xs = None
+    kv = []
     for j, layer in enumerate(layers):
         n_sub = len(layer)
         if j == 0:
@@ -156,13 +176,99 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
             if len(xs) != n_sub:
                 raise ValueError("every layer must have the same number of sub-layers")
             y = np.sum(xs, axis=0)
-        xs = [sub_layer_forward(xs[i], y, layer[i], cu_seqlens, n_heads, eps)
+        kv_j = []
+        xs = [sub_layer_forward(xs[i], y, layer[i], cu_seqlens, n_heads, eps,
+                                kv_j if return_kv else None)
               for i in range(n_sub)]
+        kv.append(kv_j)
     if xs is None:
         raise ValueError("at least one layer is required")
     Y = np.concatenate(xs, axis=1)          # [T, N*d]
     out = Y @ _f64(W_concat)
+    if return_kv:
+        return out, np.stack(xs), kv
     return out, np.stack(xs)
+
+
+def cached_attention(q, k_new, v_new, K_cache, V_cache, n_heads: int) -> np.ndarray:
+    """Attention of one new token per sequence over its cached keys and its own.
+
+    ``q, k_new, v_new`` are ``[B, d]`` (row b: the new token of sequence b);
+    ``K_cache[b], V_cache[b]`` are ``[S_b, d]`` (the earlier tokens, ``S_b >= 0``).
+    Row b attends to the ``S_b + 1`` keys ``[K_cache[b]; k_new[b]]`` with the scaled
+    dot-product softmax of Section 2.1 (no mask is needed: every cached token precedes
+    the new one).  Returns ``[B, d]``, heads concatenated.
+    """
+    q, k_new, v_new = _f64(q), _f64(k_new), _f64(v_new)
+    B, d = q.shape
+    hd = d // n_heads
+    out = np.zeros((B, d), dtype=np.float64)
+    for b in range(B):
+        Kb = np.concatenate([_f64(K_cache[b]).reshape(-1, d), k_new[b:b + 1]], axis=0)
+        Vb = np.concatenate([_f64(V_cache[b]).reshape(-1, d), v_new[b:b + 1]], axis=0)
+        for h in range(n_heads):
+            cols = slice(h * hd, (h + 1) * hd)
+            scores = Kb[:, cols] @ q[b, cols] / math.sqrt(hd)
+            scores -= scores.max()
+            p = np.exp(scores)
+            out[b, cols] = (p / p.sum()) @ Vb[:, cols]
+    return out
+
+
+def kraken_decode(X_new, kv_cache, layers: Iterable[Sequence[Mapping]], W_concat,
+                  n_heads: int, eps: float = LN_EPS):
+    """One decode step: the next token of each of B sequences through the stack.
+
+    ``X_new`` is ``[B, d]`` (row b: the new token of sequence b; its first-layer
+    input, shared by the N sub-layers as in the prefill).  ``kv_cache[j][i] =
+    (K, V)`` where ``K[b], V[b]`` are the ``[S_b, d]`` keys and values of sequence
+    b's earlier tokens at layer j, sub-layer i.  Each layer runs Algorithm 1 on the
+    new rows (combine ``y`` as in the prefill: ``X_new`` at the first layer, else the
+    sum of the N previous outputs), the attention being ``cached_attention``.
+
+    Returns ``(out [B, d], sub_out [N, B, d], kv_new)`` with ``kv_new[j][i] = (k, v)``,
+    the new tokens' keys and values (``[B, d]`` each), which a following step appends.
+    """
+    X = _f64(X_new)
+    xs = None
+    kv_new = []
+    for j, layer in enumerate(layers):
+        n_sub = len(layer)
+        y = X if j == 0 else np.sum(xs, axis=0)
+        if j == 0:
+            xs = [X] * n_sub
+        nxt, kv_j = [], []
+        for i in range(n_sub):
+            p = layer[i]
+            x = xs[i]
+            d = x.shape[1]
+            u = layer_norm(x, p["ln1_g"], p["ln1_b"], eps)
+            qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
+            q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+            kv_j.append((k, v))
+            K_c, V_c = kv_cache[j][i]
+            a = cached_attention(q, k, v, K_c, V_c, n_heads)
+            h = x + a @ _f64(p["Wo"]) + _f64(p["bo"])
+            nxt.append(h + feed_forward(layer_norm(h + y, p["ln2_g"], p["ln2_b"], eps), p))
+        xs = nxt
+        kv_new.append(kv_j)
+    if xs is None:
+        raise ValueError("at least one layer is required")
+    out = np.concatenate(xs, axis=1) @ _f64(W_concat)
+    return out, np.stack(xs), kv_new
+
+
+def split_kv(kv, cu_seqlens: Sequence[int]):
+    """Per-sequence view of a prefill's keys and values: ``kv[j][i] = (K, V)`` with
+    ``K, V [T, d]`` -> ``(K_list, V_list)`` with one ``[S_b, d]`` block per sequence."""
+    out = []
+    for kv_j in kv:
+        row = []
+        for K, V in kv_j:
+            row.append(([K[cu_seqlens[b]:cu_seqlens[b + 1]] for b in range(len(cu_seqlens) - 1)],
+                        [V[cu_seqlens[b]:cu_seqlens[b + 1]] for b in range(len(cu_seqlens) - 1)]))
+        out.append(row)
+    return out
 
 
 def kraken_param_count(n_sub: int, n_layers: int, d: int, d_ff: int,

@@ -405,3 +405,98 @@ def test_p13_model_totals():
         no_cat = O.kraken_param_count(n_sub, L, d, 2 * d, vocab=50257, positions=1024,
                                       biases=False, layer_norms=False, w_concat=False) / 1e6
         assert printed - no_cat > 0.35
+
+
+# ---------------------------------- decode: one token past a cached prefix (Section 2.1)
+#
+# The decode oracle is pinned to the (already pinned) prefill oracle by causality: the
+# new token's row of a prefill over the extended sequence is exactly what a decode step
+# over the prefix's cached keys and values must produce, and the extended prefill's keys
+# and values are the prefix's plus the decode step's.  The cached attention itself is
+# checked against the explicit-loop brute force above.
+
+def _stack(rng, n_sub, n_layers, d, f, affine=True, scale=0.3):
+    return [[rand_params(rng, d, f, scale=scale, affine=affine) for _ in range(n_sub)]
+            for _ in range(n_layers)]
+
+
+def _decode_case(seed=5, n_sub=2, n_layers=3, d=8, f=16, H=2, lens=(5, 1, 3)):
+    rng = np.random.default_rng(seed)
+    layers = _stack(rng, n_sub, n_layers, d, f)
+    wcat = rng.normal(0, 0.3, (n_sub * d, d))
+    X_full = [rng.normal(0, 1, (S + 2, d)) for S in lens]   # prefix + two decode tokens
+    return layers, wcat, X_full, H
+
+
+def _prefill(seqs, layers, wcat, H):
+    cu = [0]
+    for s in seqs:
+        cu.append(cu[-1] + len(s))
+    out, sub, kv = O.kraken_prefill(np.concatenate(seqs), cu, layers, wcat, H, return_kv=True)
+    return cu, out, sub, kv
+
+
+def test_decode_step_equals_last_row_of_extended_prefill():
+    layers, wcat, X_full, H = _decode_case()
+    lens = [len(x) - 2 for x in X_full]
+    cu_p, _, _, kv_p = _prefill([x[:-2] for x in X_full], layers, wcat, H)
+    cu_e, out_e, sub_e, _ = _prefill([x[:-1] for x in X_full], layers, wcat, H)
+    X_new = np.stack([x[-2] for x in X_full])
+    out_d, sub_d, _ = O.kraken_decode(X_new, O.split_kv(kv_p, cu_p), layers, wcat, H)
+    last = [cu_e[b + 1] - 1 for b in range(len(lens))]
+    assert rel_err(out_d, out_e[last]) < 1e-12
+    assert rel_err(sub_d, sub_e[:, last]) < 1e-12
+
+
+def test_two_decode_steps_equal_extended_prefill_and_its_cache():
+    layers, wcat, X_full, H = _decode_case(seed=11, lens=(4, 2))
+    cu_p, _, _, kv_p = _prefill([x[:-2] for x in X_full], layers, wcat, H)
+    cu_e, out_e, sub_e, kv_e = _prefill(X_full, layers, wcat, H)
+    cache = O.split_kv(kv_p, cu_p)
+    outs = []
+    for step in (2, 1):
+        X_new = np.stack([x[-step] for x in X_full])
+        out_d, _, kv_new = O.kraken_decode(X_new, cache, layers, wcat, H)
+        outs.append(out_d)
+        # append the step's keys and values to each sequence's cache
+        cache = [[([np.vstack([Kc[b], kv_new[j][i][0][b:b + 1]]) for b in range(len(Kc))],
+                   [np.vstack([Vc[b], kv_new[j][i][1][b:b + 1]]) for b in range(len(Vc))])
+                  for i, (Kc, Vc) in enumerate(row)] for j, row in enumerate(cache)]
+    for k, step in enumerate((2, 1)):
+        rows = [cu_e[b + 1] - step for b in range(len(X_full))]
+        assert rel_err(outs[k], out_e[rows]) < 1e-12
+    # the cache after two steps is the extended prefill's keys and values
+    full = O.split_kv(kv_e, cu_e)
+    for j in range(len(layers)):
+        for i in range(len(layers[0])):
+            for b in range(len(X_full)):
+                assert rel_err(cache[j][i][0][b], full[j][i][0][b]) < 1e-12
+                assert rel_err(cache[j][i][1][b], full[j][i][1][b]) < 1e-12
+
+
+def test_decode_with_empty_cache_is_a_one_token_prefill():
+    layers, wcat, X_full, H = _decode_case(seed=2, lens=(0, 0))
+    d = X_full[0].shape[1]
+    empty = [[([np.zeros((0, d))] * 2, [np.zeros((0, d))] * 2) for _ in row] for row in layers]
+    X_new = np.stack([x[0] for x in X_full])
+    out_d, sub_d, _ = O.kraken_decode(X_new, empty, layers, wcat, H)
+    cu = [0, 1, 2]
+    out_p, sub_p = O.kraken_prefill(X_new, cu, layers, wcat, H)
+    assert rel_err(out_d, out_p) < 1e-12 and rel_err(sub_d, sub_p) < 1e-12
+
+
+def test_cached_attention_matches_brute_force():
+    rng = np.random.default_rng(7)
+    d, H = 6, 3
+    lens = [4, 0, 2]
+    Kc = [rng.normal(0, 1, (S, d)) for S in lens]
+    Vc = [rng.normal(0, 1, (S, d)) for S in lens]
+    q, k, v = (rng.normal(0, 1, (len(lens), d)) for _ in range(3))
+    got = O.cached_attention(q, k, v, Kc, Vc, H)
+    for b, S in enumerate(lens):
+        # the new token is the last of a sequence [cache; new]: brute force over it
+        Q = [list(r) for r in np.vstack([np.zeros((S, d)), q[b:b + 1]])]
+        K = [list(r) for r in np.vstack([Kc[b], k[b:b + 1]])]
+        V = [list(r) for r in np.vstack([Vc[b], v[b:b + 1]])]
+        ref = brute_attention(Q, K, V, [0, S + 1], H)[S]
+        assert rel_err(got[b], ref) < 1e-12
