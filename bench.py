@@ -11,6 +11,10 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--compute f16|bf16] [--no-cpu-baseline]
        python bench.py --pmc-probe      (one prefill + one 1 GiB device copy, untimed:
                                           the command the HBM counter runs profile)
+       python bench.py --phase decode [--batch B] [--context C]
+                                        (one decode step of B sequences of C cached
+                                          tokens each: decode tokens/s and an HBM
+                                          roofline of its dominant kernel)
 """
 
 import argparse
@@ -92,6 +96,129 @@ def traffic_of(kernel):
         "algorithmic": t["algorithmic_bytes"], "profile": t["profile"]}
 
 
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E
+
+
+def decode_class_bytes(w, es, B, ctx):
+    """Algorithmic HBM bytes of one decode step per kernel class: every weight matrix
+    read once in the operand type (es bytes), each sequence's cached keys and values
+    of ctx + 1 positions read once, the new keys and values written once, fp32
+    activations of the B rows read and written once per kernel."""
+    N, L, d, F = w.n_sub, w.n_layers, w.d_model, w.d_ff
+    act = lambda cols: B * cols * 4
+    return {
+        "ln1": L * (act(N * d) + B * N * d * es),
+        "gemm_qk": L * N * (2 * d * d * es + B * d * es + B * 2 * d * es),
+        "gemm_vt": L * N * (d * d * es + B * d * es + B * d * es),
+        "kv_cache": L * N * B * 2 * d * es * 2,
+        "attention": L * N * (B * (ctx + 1) * 2 * d * es + B * 2 * d * es + B * d * es),
+        "gemm_o": L * N * (d * d * es + B * d * es + 2 * act(d)),
+        "combine_ln2": L * (2 * N * act(d) + N * B * d * es),
+        "gemm_up": L * N * (F * d * es + B * d * es + B * F * es),
+        "gemm_down": L * N * (d * F * es + B * F * es + 2 * act(d)),
+        "w_concat": N * d * d * es + 2 * N * act(d) + act(d),
+    }
+
+
+def bench_decode(args, w, compute):
+    """One decode step of B sequences, each with `context` cached tokens (stand-in
+    values ~ N(0, 1) in the cache; the step's cost does not depend on them)."""
+    import torch
+
+    from paper_2408_07802_amd import kraken, synth
+
+    B, ctx = args.batch, args.context
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    cfg = kraken.Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
+                        n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=max(B, 8192), dtype=w.dtype,
+                        compute=w.compute)
+    log(f"[bench decode] {w.name} B={B} context={ctx} compute={compute}")
+    model = kraken.Kraken(cfg)
+    blob = kraken.pack_weights((synth.gen_layer(w, j, 0, dev) for j in range(w.n_layers)),
+                               synth.gen_w_concat(w, 0, dev), cfg, device=dev)
+    model.load_weights(blob)
+    torch.cuda.synchronize()
+    del blob
+    torch.cuda.empty_cache()
+    cache = model.new_kv_cache(B, ctx + 1)
+    flat = cache.buf.view(synth.compute_dtype(w))
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    step = 1 << 28
+    for o in range(0, flat.numel(), step):
+        flat[o:o + step].normal_(generator=g)
+    X = synth.gen_hidden(w, B, 0, dev)
+    out = torch.empty((B, w.d_model), dtype=torch.float32, device=dev)
+    lens = [ctx] * B
+    for _ in range(args.warmup):
+        model.decode(X, lens, cache, out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        model.decode(X, lens, cache, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench decode] {args.steps} steps: {ms_per_step:.3f} ms/step")
+
+    model.profile_reset()
+    model.profile_enable(True)
+    for _ in range(args.steps):
+        model.decode(X, lens, cache, out=out)
+    torch.cuda.synchronize()
+    prof = model.profile_read()
+    model.profile_enable(False)
+    model.close()
+
+    es = 4 if compute == "f32" else 2
+    cb = decode_class_bytes(w, es, B, ctx)
+    kernels = {}
+    for name, (ms, n) in prof.items():
+        if n == 0:
+            continue
+        by = cb.get(name)
+        per_launch = by / (n / args.steps) if by else None
+        kernels[name] = {"ms_per_step": ms / args.steps, "launches_per_step": n // args.steps,
+                         "avg_launch_ms": ms / n,
+                         "gbs": per_launch / (ms / n * 1e-3) / 1e9 if by else None}
+    dominant = max((k for k in kernels if kernels[k]["gbs"] is not None),
+                   key=lambda k: kernels[k]["ms_per_step"])
+    dk = kernels[dominant]
+    total_bytes = sum(cb.values())
+    result = {
+        "metric": "decode tokens/s (one new token per sequence, all N sub-layers, 1 MI355X)",
+        "value": B / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": compute,
+        "data": "synthetic",
+        "config": {"workload": w.name + "-decode", "batch": B, "context": ctx,
+                   "n_sub": w.n_sub, "n_layers": w.n_layers, "d_model": w.d_model,
+                   "n_heads": w.n_heads, "d_ff": w.d_ff, "storage_dtype": w.dtype,
+                   "mfma_operands": compute, "kv_cache_bytes": cache.buf.numel()},
+        "hbm_bytes_per_step": total_bytes,
+        "hbm_util_pct": 100.0 * total_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": dk["gbs"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dk["gbs"] / HBM_PEAK_GBS,
+                     "traffic": None, "avg_launch_ms": dk["avg_launch_ms"],
+                     "launches_per_step": dk["launches_per_step"]},
+        "kernels": kernels,
+        "wall_ms_per_step": wall / args.steps * 1e3,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,6 +229,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="one prefill and one 1 GiB device copy, untimed (for HBM counters)")
+    ap.add_argument("--phase", choices=["prefill", "decode"], default="prefill")
+    ap.add_argument("--batch", type=int, default=1, help="decode: sequences per step")
+    ap.add_argument("--context", type=int, default=8192, help="decode: cached tokens each")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -119,6 +249,9 @@ def main():
     if args.compute:
         w = dataclasses.replace(w, compute=args.compute)
     compute = w.dtype if w.compute == "storage" else w.compute
+    if args.phase == "decode":
+        bench_decode(args, w, compute)
+        return
     lens = synth.seq_lens(w)
     cu = synth.cu_seqlens(lens)
     T = cu[-1]

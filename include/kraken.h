@@ -165,6 +165,61 @@ kraken_status kraken_load_weights(kraken_model* m, const void* blob, size_t nbyt
 kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
                              int32_t num_seqs, float* hidden_out, float* sub_out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * KV cache and one-token decode (Section 2.1, KV cache: the keys and values
+ * of every processed token are kept so that later tokens attend to them
+ * without recomputing them).  Every sub-layer of every layer has its own
+ * keys and values.
+ *
+ * Cache: caller-owned device memory of kraken_kv_cache_bytes(cfg, max_seqs,
+ * capacity) bytes, 16-byte aligned, elements of the MFMA operand type (the
+ * compute type; the storage type when compute is KRAKEN_COMPUTE_STORAGE):
+ *   [L][N][2 (K, V)][max_seqs][n_heads][capacity][hd]
+ * Slot b holds sequence b; position p of slot b holds the key (value) row of
+ * that sequence's p-th token, projection bias included, as the attention of
+ * kraken_prefill consumes it.  Positions at or above a sequence's length
+ * are never read.
+ *
+ * Returns 0 for an invalid cfg, max_seqs outside 1..KRAKEN_MAX_SEQS or a
+ * capacity below 1.
+ */
+size_t kraken_kv_cache_bytes(const kraken_config* cfg, int32_t max_seqs, int32_t capacity);
+
+/*
+ * kraken_prefill that also fills the cache: sequence b of the packed batch
+ * (cu_seqlens as for kraken_prefill) writes positions 0 .. S_b - 1 of slot b
+ * (S_b = cu[b+1] - cu[b] <= capacity, num_seqs <= max_seqs).  Other slots
+ * and positions are left as they are.  hidden_out and sub_out are those of
+ * kraken_prefill, bit for bit.  The cache must not overlap the other
+ * buffers.  Errors: those of kraken_prefill; INVALID_ARG for a null or
+ * misaligned cache, a sequence longer than capacity, num_seqs > max_seqs.
+ */
+kraken_status kraken_prefill_kv(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
+                                int32_t num_seqs, float* hidden_out, float* sub_out,
+                                void* kv_cache, int32_t max_seqs, int32_t capacity, void* stream);
+
+/*
+ * One decode step for num_seqs sequences, one new token each: the new token
+ * of sequence b sits at position lens[b] (the number of tokens slot b
+ * already holds), attends causally to positions 0 .. lens[b] of slot b, and
+ * its keys and values are written to position lens[b] (the cache then holds
+ * lens[b] + 1 tokens of slot b; the caller advances lens).  The result
+ * equals row lens[b] of a kraken_prefill over the sequence extended by the
+ * new token (causality, Section 2.1), up to rounding.
+ *   hidden_in   device [num_seqs][d], model dtype: the new tokens' X rows.
+ *   lens        HOST int32[num_seqs], 0 <= lens[b] < capacity.
+ *   num_seqs    1 .. min(max_seqs, max_tokens); sequence b uses slot b.
+ *   hidden_out  device float32 [num_seqs][d].
+ *   sub_out     NULL or device float32 [N][num_seqs][d].
+ * The model's workspace holds the step's activations and the attention's
+ * per-chunk partial results; one model runs one call at a time.
+ * Errors: INVALID_ARG (null or misaligned pointers, lens out of range,
+ * overlapping buffers), STATE (weights not loaded), HIP.
+ */
+kraken_status kraken_decode(kraken_model* m, const void* hidden_in, const int32_t* lens,
+                            int32_t num_seqs, float* hidden_out, float* sub_out, void* kv_cache,
+                            int32_t max_seqs, int32_t capacity, void* stream);
+
 /* Waits for the model's device work, frees everything it owns.  NULL is a no-op. */
 kraken_status kraken_destroy(kraken_model* m);
 
@@ -189,7 +244,8 @@ enum {
   KRAKEN_K_GEMM_DOWN = 7,  /* FFN down projection + residual */
   KRAKEN_K_CONCAT = 8,     /* W_concat (and its operand split) */
   KRAKEN_K_OTHER = 9,      /* input conversion, output copies */
-  KRAKEN_K_COUNT = 10
+  KRAKEN_K_KV = 10,        /* KV cache writes (kraken_prefill_kv, kraken_decode) */
+  KRAKEN_K_COUNT = 11
 };
 kraken_status kraken_profile_enable(kraken_model* m, int enable);
 kraken_status kraken_profile_read(kraken_model* m, int kernel_class, double* total_ms,
@@ -254,6 +310,29 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
                                   int32_t n, int32_t d, int32_t n_heads,
                                   const int32_t* cu_seqlens, int32_t num_seqs, void* stream);
+
+/*
+ * kraken_op_decode_attention (Section 2.1, attention of one new token per
+ * sequence over its KV cache; the kernels kraken_decode launches):
+ *   qk       S [n][B][2d]: row b's Q half (columns 0..d-1) is the new token's
+ *            query of sequence b (B = num_seqs); the K half is not read.
+ *   kv_layer S, one layer of a KV cache as kraken.h lays it out,
+ *            [n][2][max_seqs][n_heads][capacity][hd], holding keys and values
+ *            at positions 0 .. lens[b] of slot b (the new token's own at lens[b]).
+ *   out      S [n][B][d]: softmax(q K^T / sqrt(hd)) V per head over those
+ *            lens[b] + 1 positions.
+ *   lens     HOST int32[num_seqs], 0 <= lens[b] < capacity.
+ *   work     device float32 scratch of work_floats elements, at least
+ *            n * B * n_heads * (hd + 2): per-chunk (max, sum, output) partials.
+ *            The key range is split into as many chunks (multiples of 256 keys)
+ *            as the scratch holds; the result does not depend on the split
+ *            beyond rounding.
+ */
+kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const void* kv_layer,
+                                         void* out, int32_t n, int32_t d, int32_t n_heads,
+                                         const int32_t* lens, int32_t num_seqs, int32_t max_seqs,
+                                         int32_t capacity, float* work, int64_t work_floats,
+                                         void* stream);
 
 #ifdef __cplusplus
 }

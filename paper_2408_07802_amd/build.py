@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, "libkraken.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm.hip", "attention.hip", "norm.hip", "runtime.hip"]
+SOURCES = ["gemm.hip", "attention.hip", "norm.hip", "decode.hip", "runtime.hip"]
 
 COMMON_FLAGS = [
     "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}",

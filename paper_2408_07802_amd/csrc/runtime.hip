@@ -95,6 +95,7 @@ struct kraken_model {
   // workspace
   float *X32 = nullptr, *xbuf = nullptr, *hbuf = nullptr;
   void *act = nullptr, *qk = nullptr, *vt = nullptr, *o = nullptr, *g = nullptr;
+  char* ws_end = nullptr;
   // per-kernel timing
   bool prof = false;
   std::vector<ProfRec> pending;
@@ -236,9 +237,11 @@ size_t carve_workspace(kraken_model* m, void* base) {
   m->hbuf = (float*)c.take(N * T * d * 4);
   m->act = c.take(N * T * d * es);
   m->qk = c.take(N * T * 2 * d * es);
-  m->vt = c.take(N * d * (size_t)vt_ld(m->Tmax) * es);
   m->o = c.take(N * T * d * es);
+  // vt and g stay adjacent and last: a decode step keeps its attention partials there
+  m->vt = c.take(N * d * (size_t)vt_ld(m->Tmax) * es);
   m->g = c.take(std::max(N * T * F, 2 * N * T * d) * es);
+  m->ws_end = base ? static_cast<char*>(base) + c.off : nullptr;
   return c.off;
 }
 
@@ -289,6 +292,196 @@ GemmDesc gemm_base(DType dt) {
   g.kgroups = 1;
   g.gBmod = 1;
   return g;
+}
+
+// KV cache of a prefill_kv or decode call.  cache points at layer 0; layer j starts
+// j * layer_bytes further.  lens is set for a decode step (host, one entry per sequence).
+struct KvRef {
+  char* cache = nullptr;
+  size_t layer_bytes = 0;
+  int max_seqs = 0, cap = 0;
+  const int32_t* lens = nullptr;
+};
+
+size_t kv_layer_bytes(const kraken_model* m, int max_seqs, int cap) {
+  return (size_t)m->N * 2 * (size_t)max_seqs * (size_t)cap * (size_t)m->d * sz(m->dt);
+}
+
+// fp32 elements available to a decode step's attention partials: the vt and g regions.
+int64_t decode_partial_room(const kraken_model* m) {
+  return (int64_t)((m->ws_end - static_cast<char*>(m->vt)) / sizeof(float));
+}
+
+// The whole pass over T rows, validated by the caller.  Prefill: T packed tokens of
+// num_seqs sequences (cu), causal attention within each; with kv, each layer's K and V
+// also go to the cache.  Decode (kv->lens set): T = num_seqs new tokens, one per
+// sequence; each layer appends its K and V to the cache and attends over it.
+kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32_t* cu,
+                      int32_t num_seqs, const KvRef* kv, float* hidden_out, float* sub_out,
+                      hipStream_t s) {
+  const bool decode = kv && kv->lens;
+  const DType dt = m->dt;
+  const int64_t N = m->N, d = m->d, F = m->F;
+  const int64_t Td = (int64_t)T * d;
+  const int ldv = vt_ld(T);
+  hipError_t e;
+#define RUN(cls, call, what)                      \
+  do {                                            \
+    e = m->run(cls, s, [&]() { return (call); }); \
+    if (e != hipSuccess) return hip_fail(e, what); \
+  } while (0)
+
+  const float* X32 = static_cast<const float*>(hidden_in);
+  if (m->st != DType::F32) {
+    RUN(KRAKEN_K_OTHER, launch_to_f32(m->st, hidden_in, m->X32, Td, s), "input conversion");
+    X32 = m->X32;
+  }
+
+  // Attention reads V^T in 16-byte chunks of 8 tokens; the padding columns [T, ldv) are
+  // only ever multiplied by zero probabilities but must hold finite values.
+  if (!decode && ldv > T)
+    RUN(KRAKEN_K_OTHER, launch_zero_cols(dt, m->vt, N * d, ldv, T, ldv, s), "V padding");
+
+  for (int j = 0; j < m->L; ++j) {
+    const LayerW& w = m->layers[j];
+    const float* xin = j == 0 ? X32 : m->xbuf;   // sub-layer inputs x_i
+    const int64_t xs = j == 0 ? 0 : Td;           // first layer: one shared input
+    char* cache_j = kv ? kv->cache + (size_t)j * kv->layer_bytes : nullptr;
+    RUN(KRAKEN_K_LN1,
+        launch_layernorm(dt, xin, xs, w.ln1_g, w.ln1_b, m->act, (int)N, T, (int)d, m->eps, s),
+        "ln1");
+    {
+      GemmDesc g = gemm_base(dt);
+      g.epi = EPI_BIAS_N;
+      g.A = m->act; g.lda = (int)d; g.sA = Td;
+      g.B = w.WqkT; g.ldb = (int)d; g.sB = 2 * d * d;
+      g.C = m->qk; g.ldc = (int)(2 * d); g.sC = 2 * Td;
+      g.bias = w.bqk; g.sBias = 2 * d;
+      g.M = T; g.N = (int)(2 * d); g.K = (int)d; g.batch = (int)N;
+      RUN(KRAKEN_K_GEMM_QK, launch_gemm(g, s), "QK projection");
+    }
+    if (!decode) {
+      {
+        GemmDesc g = gemm_base(dt);
+        g.epi = EPI_BIAS_M;
+        g.A = w.WvT; g.lda = (int)d; g.sA = d * d;
+        g.B = m->act; g.ldb = (int)d; g.sB = Td;
+        g.C = m->vt; g.ldc = ldv; g.sC = d * ldv;
+        g.bias = w.bv; g.sBias = d;
+        g.M = (int)d; g.N = T; g.K = (int)d; g.batch = (int)N;
+        RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
+      }
+      if (kv)
+        RUN(KRAKEN_K_KV,
+            launch_kv_store(dt, m->qk, m->vt, cache_j, (int)N, T, (int)d, m->H, cu, num_seqs,
+                            kv->max_seqs, kv->cap, s),
+            "KV store");
+      AttnDesc a;
+      a.dt = dt; a.qk = m->qk; a.vt = m->vt; a.out = m->o;
+      a.n = (int)N; a.T = T; a.d = (int)d; a.n_heads = m->H;
+      a.cu_host = cu; a.num_seqs = num_seqs;
+      RUN(KRAKEN_K_ATTN, launch_attention(a, s), "attention");
+    } else {
+      // V rows of the new tokens go through o ([N][T][d]) into the cache; o then takes
+      // the attention output, after the append has read it (stream order).
+      {
+        GemmDesc g = gemm_base(dt);
+        g.epi = EPI_BIAS_N;
+        g.A = m->act; g.lda = (int)d; g.sA = Td;
+        g.B = w.WvT; g.ldb = (int)d; g.sB = d * d;
+        g.C = m->o; g.ldc = (int)d; g.sC = Td;
+        g.bias = w.bv; g.sBias = d;
+        g.M = T; g.N = (int)d; g.K = (int)d; g.batch = (int)N;
+        RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
+      }
+      RUN(KRAKEN_K_KV,
+          launch_kv_append(dt, m->qk, m->o, cache_j, (int)N, T, (int)d, m->H, kv->lens,
+                           kv->max_seqs, kv->cap, s),
+          "KV append");
+      RUN(KRAKEN_K_ATTN,
+          launch_decode_attention(dt, m->qk, cache_j, static_cast<float*>(m->vt),
+                                  decode_partial_room(m), m->o, (int)N, T, (int)d, m->H,
+                                  kv->lens, kv->max_seqs, kv->cap, s),
+          "decode attention");
+    }
+    {
+      GemmDesc g = gemm_base(dt);
+      g.epi = EPI_BIAS_N_RES;
+      g.A = m->o; g.lda = (int)d; g.sA = Td;
+      g.B = w.WoT; g.ldb = (int)d; g.sB = d * d;
+      g.C = m->hbuf; g.ldc = (int)d; g.sC = Td;
+      g.bias = w.bo; g.sBias = d;
+      g.R = xin; g.sR = xs;
+      g.M = T; g.N = (int)d; g.K = (int)d; g.batch = (int)N;
+      RUN(KRAKEN_K_GEMM_O, launch_gemm(g, s), "output projection");
+    }
+    RUN(KRAKEN_K_COMBINE,
+        launch_combine_ln2(dt, m->xbuf, j == 0 ? X32 : nullptr, m->hbuf, w.ln2_g, w.ln2_b, m->act,
+                           (int)N, T, (int)d, m->eps, s),
+        "combine + ln2");
+    {
+      GemmDesc g = gemm_base(dt);
+      g.epi = EPI_BIAS_N_GELU;
+      g.A = m->act; g.lda = (int)d; g.sA = Td;
+      g.B = w.W1T; g.ldb = (int)d; g.sB = F * d;
+      g.C = m->g; g.ldc = (int)F; g.sC = (int64_t)T * F;
+      g.bias = w.b1; g.sBias = F;
+      g.M = T; g.N = (int)F; g.K = (int)d; g.batch = (int)N;
+      RUN(KRAKEN_K_GEMM_UP, launch_gemm(g, s), "FFN up");
+    }
+    {
+      GemmDesc g = gemm_base(dt);
+      g.epi = EPI_BIAS_N_RES;
+      g.A = m->g; g.lda = (int)F; g.sA = (int64_t)T * F;
+      g.B = w.W2T; g.ldb = (int)F; g.sB = d * F;
+      g.C = m->xbuf; g.ldc = (int)d; g.sC = Td;
+      g.bias = w.b2; g.sBias = d;
+      g.R = m->hbuf; g.sR = Td;
+      g.M = T; g.N = (int)d; g.K = (int)F; g.batch = (int)N;
+      RUN(KRAKEN_K_GEMM_DOWN, launch_gemm(g, s), "FFN down");
+    }
+  }
+
+  if (sub_out)
+    RUN(KRAKEN_K_OTHER,
+        hipMemcpyAsync(sub_out, m->xbuf, N * Td * sizeof(float), hipMemcpyDeviceToDevice, s),
+        "sub_out copy");
+
+  // out = [Y_1 | ... | Y_N] W_concat, K split into N groups of d (one per sub-layer).
+  {
+    GemmDesc g = gemm_base(dt);
+    g.epi = EPI_BIAS_N_RES;
+    if (dt != DType::F32) {
+      // 16-bit operands: Y = hi + lo with hi = S(Y), lo = S(Y - hi); 2N groups
+      RUN(KRAKEN_K_CONCAT, launch_split16(dt, m->xbuf, m->g, N * Td, s),
+          "W_concat operand split");
+      g.A = m->g;
+      g.kgroups = (int)(2 * N);
+    } else {
+      g.A = m->xbuf;
+      g.kgroups = (int)N;
+    }
+    g.lda = (int)d; g.gA = Td;
+    g.B = m->WcatT; g.ldb = (int)(N * d); g.gB = d; g.gBmod = (int)N;
+    g.C = hidden_out; g.ldc = (int)d;
+    g.M = T; g.N = (int)d; g.K = (int)d;
+    RUN(KRAKEN_K_CONCAT, launch_gemm(g, s), "W_concat");
+  }
+#undef RUN
+  return KRAKEN_OK;
+}
+
+// Checks shared by prefill_kv and decode: a cache for this model's sizes.
+kraken_status check_cache(const kraken_model* m, const void* cache, int32_t max_seqs,
+                          int32_t capacity, int32_t num_seqs, size_t* bytes) {
+  if (!cache) return fail(KRAKEN_ERR_INVALID_ARG, "kv_cache is NULL");
+  if (reinterpret_cast<uintptr_t>(cache) % 16 != 0)
+    return fail(KRAKEN_ERR_INVALID_ARG, "kv_cache is not 16-byte aligned");
+  if (max_seqs < 1 || max_seqs > KRAKEN_MAX_SEQS || capacity < 1)
+    return fail(KRAKEN_ERR_INVALID_ARG, "max_seqs out of 1..KRAKEN_MAX_SEQS or capacity < 1");
+  if (num_seqs > max_seqs) return fail(KRAKEN_ERR_INVALID_ARG, "num_seqs exceeds max_seqs");
+  *bytes = kv_layer_bytes(m, max_seqs, capacity) * (size_t)m->L;
+  return KRAKEN_OK;
 }
 
 }  // namespace
@@ -456,6 +649,22 @@ kraken_status kraken_load_weights(kraken_model* m, const void* blob, size_t nbyt
 
 kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
                              int32_t num_seqs, float* hidden_out, float* sub_out, void* stream) {
+  return kraken_prefill_kv(m, hidden_in, cu_seqlens, num_seqs, hidden_out, sub_out, nullptr, 0, 0,
+                           stream);
+}
+
+size_t kraken_kv_cache_bytes(const kraken_config* c, int32_t max_seqs, int32_t capacity) {
+  if (!c || validate_cfg(c) != KRAKEN_OK) return 0;
+  if (max_seqs < 1 || max_seqs > KRAKEN_MAX_SEQS || capacity < 1) return 0;
+  const DType st = (DType)c->dtype;
+  const DType dt = c->compute == KRAKEN_COMPUTE_STORAGE ? st : (DType)(c->compute - 1);
+  return (size_t)c->n_layers * (size_t)c->n_sub * 2 * (size_t)max_seqs * (size_t)capacity *
+         (size_t)c->d_model * sz(dt);
+}
+
+kraken_status kraken_prefill_kv(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
+                                int32_t num_seqs, float* hidden_out, float* sub_out,
+                                void* kv_cache, int32_t max_seqs, int32_t capacity, void* stream) {
   if (!m) return fail(KRAKEN_ERR_INVALID_ARG, "model is NULL");
   if (!hidden_in || !hidden_out) return fail(KRAKEN_ERR_INVALID_ARG, "hidden_in or hidden_out is NULL");
   if (!m->loaded) return fail(KRAKEN_ERR_STATE, "weights are not loaded");
@@ -463,136 +672,74 @@ kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32
   kraken_status st = check_cu(cu_seqlens, num_seqs, m->Tmax, &T64);
   if (st != KRAKEN_OK) return st;
   const int T = (int)T64;
-  const int64_t N = m->N, d = m->d, F = m->F;
+  const int64_t N = m->N, d = m->d;
   const size_t in_bytes = T * d * sz(m->st), out_bytes = T * d * 4, sub_bytes = N * T * d * 4;
   if (overlap(hidden_in, in_bytes, hidden_out, out_bytes) ||
       overlap(hidden_in, in_bytes, sub_out, sub_bytes) ||
       overlap(hidden_out, out_bytes, sub_out, sub_bytes))
     return fail(KRAKEN_ERR_INVALID_ARG, "input and output buffers overlap");
+  KvRef kv;
+  const bool with_kv = kv_cache != nullptr;
+  if (with_kv) {
+    size_t cbytes = 0;
+    st = check_cache(m, kv_cache, max_seqs, capacity, num_seqs, &cbytes);
+    if (st != KRAKEN_OK) return st;
+    for (int b = 0; b < num_seqs; ++b)
+      if (cu_seqlens[b + 1] - cu_seqlens[b] > capacity)
+        return fail(KRAKEN_ERR_INVALID_ARG, "a sequence is longer than the cache capacity");
+    if (overlap(kv_cache, cbytes, hidden_in, in_bytes) ||
+        overlap(kv_cache, cbytes, hidden_out, out_bytes) ||
+        overlap(kv_cache, cbytes, sub_out, sub_bytes))
+      return fail(KRAKEN_ERR_INVALID_ARG, "kv_cache overlaps another buffer");
+    kv.cache = static_cast<char*>(kv_cache);
+    kv.layer_bytes = kv_layer_bytes(m, max_seqs, capacity);
+    kv.max_seqs = max_seqs;
+    kv.cap = capacity;
+  }
   st = check_device(m);
   if (st != KRAKEN_OK) return st;
+  return forward(m, hidden_in, T, cu_seqlens, num_seqs, with_kv ? &kv : nullptr, hidden_out,
+                 sub_out, static_cast<hipStream_t>(stream));
+}
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const DType dt = m->dt;
-  const int64_t Td = (int64_t)T * d;
-  const int ldv = vt_ld(T);
-  hipError_t e;
-#define RUN(cls, call, what)                      \
-  do {                                            \
-    e = m->run(cls, s, [&]() { return (call); }); \
-    if (e != hipSuccess) return hip_fail(e, what); \
-  } while (0)
-
-  const float* X32 = static_cast<const float*>(hidden_in);
-  if (m->st != DType::F32) {
-    RUN(KRAKEN_K_OTHER, launch_to_f32(m->st, hidden_in, m->X32, Td, s), "input conversion");
-    X32 = m->X32;
-  }
-
-  // Attention reads V^T in 16-byte chunks of 8 tokens; the padding columns [T, ldv) are
-  // only ever multiplied by zero probabilities but must hold finite values.
-  if (ldv > T)
-    RUN(KRAKEN_K_OTHER, launch_zero_cols(dt, m->vt, N * d, ldv, T, ldv, s), "V padding");
-
-  for (int j = 0; j < m->L; ++j) {
-    const LayerW& w = m->layers[j];
-    const float* xin = j == 0 ? X32 : m->xbuf;   // sub-layer inputs x_i
-    const int64_t xs = j == 0 ? 0 : Td;           // first layer: one shared input
-    RUN(KRAKEN_K_LN1,
-        launch_layernorm(dt, xin, xs, w.ln1_g, w.ln1_b, m->act, (int)N, T, (int)d, m->eps, s),
-        "ln1");
-    {
-      GemmDesc g = gemm_base(dt);
-      g.epi = EPI_BIAS_N;
-      g.A = m->act; g.lda = (int)d; g.sA = Td;
-      g.B = w.WqkT; g.ldb = (int)d; g.sB = 2 * d * d;
-      g.C = m->qk; g.ldc = (int)(2 * d); g.sC = 2 * Td;
-      g.bias = w.bqk; g.sBias = 2 * d;
-      g.M = T; g.N = (int)(2 * d); g.K = (int)d; g.batch = (int)N;
-      RUN(KRAKEN_K_GEMM_QK, launch_gemm(g, s), "QK projection");
-    }
-    {
-      GemmDesc g = gemm_base(dt);
-      g.epi = EPI_BIAS_M;
-      g.A = w.WvT; g.lda = (int)d; g.sA = d * d;
-      g.B = m->act; g.ldb = (int)d; g.sB = Td;
-      g.C = m->vt; g.ldc = ldv; g.sC = d * ldv;
-      g.bias = w.bv; g.sBias = d;
-      g.M = (int)d; g.N = T; g.K = (int)d; g.batch = (int)N;
-      RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
-    }
-    {
-      AttnDesc a;
-      a.dt = dt; a.qk = m->qk; a.vt = m->vt; a.out = m->o;
-      a.n = (int)N; a.T = T; a.d = (int)d; a.n_heads = m->H;
-      a.cu_host = cu_seqlens; a.num_seqs = num_seqs;
-      RUN(KRAKEN_K_ATTN, launch_attention(a, s), "attention");
-    }
-    {
-      GemmDesc g = gemm_base(dt);
-      g.epi = EPI_BIAS_N_RES;
-      g.A = m->o; g.lda = (int)d; g.sA = Td;
-      g.B = w.WoT; g.ldb = (int)d; g.sB = d * d;
-      g.C = m->hbuf; g.ldc = (int)d; g.sC = Td;
-      g.bias = w.bo; g.sBias = d;
-      g.R = xin; g.sR = xs;
-      g.M = T; g.N = (int)d; g.K = (int)d; g.batch = (int)N;
-      RUN(KRAKEN_K_GEMM_O, launch_gemm(g, s), "output projection");
-    }
-    RUN(KRAKEN_K_COMBINE,
-        launch_combine_ln2(dt, m->xbuf, j == 0 ? X32 : nullptr, m->hbuf, w.ln2_g, w.ln2_b, m->act,
-                           (int)N, T, (int)d, m->eps, s),
-        "combine + ln2");
-    {
-      GemmDesc g = gemm_base(dt);
-      g.epi = EPI_BIAS_N_GELU;
-      g.A = m->act; g.lda = (int)d; g.sA = Td;
-      g.B = w.W1T; g.ldb = (int)d; g.sB = F * d;
-      g.C = m->g; g.ldc = (int)F; g.sC = (int64_t)T * F;
-      g.bias = w.b1; g.sBias = F;
-      g.M = T; g.N = (int)F; g.K = (int)d; g.batch = (int)N;
-      RUN(KRAKEN_K_GEMM_UP, launch_gemm(g, s), "FFN up");
-    }
-    {
-      GemmDesc g = gemm_base(dt);
-      g.epi = EPI_BIAS_N_RES;
-      g.A = m->g; g.lda = (int)F; g.sA = (int64_t)T * F;
-      g.B = w.W2T; g.ldb = (int)F; g.sB = d * F;
-      g.C = m->xbuf; g.ldc = (int)d; g.sC = Td;
-      g.bias = w.b2; g.sBias = d;
-      g.R = m->hbuf; g.sR = Td;
-      g.M = T; g.N = (int)d; g.K = (int)F; g.batch = (int)N;
-      RUN(KRAKEN_K_GEMM_DOWN, launch_gemm(g, s), "FFN down");
-    }
-  }
-
-  if (sub_out)
-    RUN(KRAKEN_K_OTHER,
-        hipMemcpyAsync(sub_out, m->xbuf, N * Td * sizeof(float), hipMemcpyDeviceToDevice, s),
-        "sub_out copy");
-
-  // out = [Y_1 | ... | Y_N] W_concat, K split into N groups of d (one per sub-layer).
-  {
-    GemmDesc g = gemm_base(dt);
-    g.epi = EPI_BIAS_N_RES;
-    if (dt != DType::F32) {
-      // 16-bit operands: Y = hi + lo with hi = S(Y), lo = S(Y - hi); 2N groups
-      RUN(KRAKEN_K_CONCAT, launch_split16(dt, m->xbuf, m->g, N * Td, s),
-          "W_concat operand split");
-      g.A = m->g;
-      g.kgroups = (int)(2 * N);
-    } else {
-      g.A = m->xbuf;
-      g.kgroups = (int)N;
-    }
-    g.lda = (int)d; g.gA = Td;
-    g.B = m->WcatT; g.ldb = (int)(N * d); g.gB = d; g.gBmod = (int)N;
-    g.C = hidden_out; g.ldc = (int)d;
-    g.M = T; g.N = (int)d; g.K = (int)d;
-    RUN(KRAKEN_K_CONCAT, launch_gemm(g, s), "W_concat");
-  }
-#undef RUN
-  return KRAKEN_OK;
+kraken_status kraken_decode(kraken_model* m, const void* hidden_in, const int32_t* lens,
+                            int32_t num_seqs, float* hidden_out, float* sub_out, void* kv_cache,
+                            int32_t max_seqs, int32_t capacity, void* stream) {
+  if (!m) return fail(KRAKEN_ERR_INVALID_ARG, "model is NULL");
+  if (!hidden_in || !hidden_out || !lens)
+    return fail(KRAKEN_ERR_INVALID_ARG, "hidden_in, hidden_out or lens is NULL");
+  if (!m->loaded) return fail(KRAKEN_ERR_STATE, "weights are not loaded");
+  if (num_seqs < 1 || num_seqs > KRAKEN_MAX_SEQS || num_seqs > m->Tmax)
+    return fail(KRAKEN_ERR_INVALID_ARG, "num_seqs out of 1..min(KRAKEN_MAX_SEQS, max_tokens)");
+  size_t cbytes = 0;
+  kraken_status st = check_cache(m, kv_cache, max_seqs, capacity, num_seqs, &cbytes);
+  if (st != KRAKEN_OK) return st;
+  for (int b = 0; b < num_seqs; ++b)
+    if (lens[b] < 0 || lens[b] >= capacity)
+      return fail(KRAKEN_ERR_INVALID_ARG, "lens[b] out of 0..capacity-1");
+  const int B = num_seqs;
+  const int64_t N = m->N, d = m->d;
+  const size_t in_bytes = B * d * sz(m->st), out_bytes = B * d * 4, sub_bytes = N * B * d * 4;
+  if (overlap(hidden_in, in_bytes, hidden_out, out_bytes) ||
+      overlap(hidden_in, in_bytes, sub_out, sub_bytes) ||
+      overlap(hidden_out, out_bytes, sub_out, sub_bytes))
+    return fail(KRAKEN_ERR_INVALID_ARG, "input and output buffers overlap");
+  if (overlap(kv_cache, cbytes, hidden_in, in_bytes) ||
+      overlap(kv_cache, cbytes, hidden_out, out_bytes) ||
+      overlap(kv_cache, cbytes, sub_out, sub_bytes))
+    return fail(KRAKEN_ERR_INVALID_ARG, "kv_cache overlaps another buffer");
+  if (decode_partial_floats((int)N, B, m->H, (int)d / m->H, 1) > decode_partial_room(m))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "workspace too small for the decode attention partials");
+  st = check_device(m);
+  if (st != KRAKEN_OK) return st;
+  KvRef kv;
+  kv.cache = static_cast<char*>(kv_cache);
+  kv.layer_bytes = kv_layer_bytes(m, max_seqs, capacity);
+  kv.max_seqs = max_seqs;
+  kv.cap = capacity;
+  kv.lens = lens;
+  return forward(m, hidden_in, B, nullptr, num_seqs, &kv, hidden_out, sub_out,
+                 static_cast<hipStream_t>(stream));
 }
 
 kraken_status kraken_profile_enable(kraken_model* m, int enable) {
@@ -729,6 +876,35 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
   a.cu_host = cu_seqlens; a.num_seqs = num_seqs;
   hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "attention");
+}
+
+kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const void* kv_layer,
+                                         void* out, int32_t n, int32_t d, int32_t n_heads,
+                                         const int32_t* lens, int32_t num_seqs, int32_t max_seqs,
+                                         int32_t capacity, float* work, int64_t work_floats,
+                                         void* stream) {
+  if (!qk || !kv_layer || !out || !lens || !work)
+    return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
+  if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
+    return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
+  if (n < 1 || d < 1 || n_heads < 1 || d % n_heads != 0)
+    return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
+  const int hd = d / n_heads;
+  if (hd != 32 && hd != 64 && hd != 128) return fail(KRAKEN_ERR_UNSUPPORTED, "head size");
+  if (num_seqs < 1 || num_seqs > KRAKEN_MAX_SEQS || max_seqs < num_seqs ||
+      max_seqs > KRAKEN_MAX_SEQS || capacity < 1)
+    return fail(KRAKEN_ERR_INVALID_ARG, "num_seqs, max_seqs or capacity out of range");
+  if (reinterpret_cast<uintptr_t>(kv_layer) % 16 != 0 || reinterpret_cast<uintptr_t>(qk) % 16 != 0)
+    return fail(KRAKEN_ERR_INVALID_ARG, "qk or kv_layer is not 16-byte aligned");
+  for (int b = 0; b < num_seqs; ++b)
+    if (lens[b] < 0 || lens[b] >= capacity)
+      return fail(KRAKEN_ERR_INVALID_ARG, "lens[b] out of 0..capacity-1");
+  if (work_floats < decode_partial_floats(n, num_seqs, n_heads, hd, 1))
+    return fail(KRAKEN_ERR_INVALID_ARG, "work is smaller than n * B * n_heads * (hd + 2)");
+  hipError_t e = launch_decode_attention((DType)dtype, qk, kv_layer, work, work_floats, out, n,
+                                         num_seqs, d, n_heads, lens, max_seqs, capacity,
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "decode attention");
 }
 
 }  // extern "C"

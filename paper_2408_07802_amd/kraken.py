@@ -25,10 +25,10 @@ MAX_SEQS = 256
 
 # kernel classes of the per-kernel timer (kraken.h)
 K_LN1, K_GEMM_QK, K_GEMM_VT, K_ATTN, K_GEMM_O, K_COMBINE, K_GEMM_UP, K_GEMM_DOWN, K_CONCAT, \
-    K_OTHER = range(10)
-K_COUNT = 10
+    K_OTHER, K_KV = range(11)
+K_COUNT = 11
 KERNEL_CLASS_NAMES = ["ln1", "gemm_qk", "gemm_vt", "attention", "gemm_o", "combine_ln2",
-                      "gemm_up", "gemm_down", "w_concat", "other"]
+                      "gemm_up", "gemm_down", "w_concat", "other", "kv_cache"]
 
 EPI_BIAS_N, EPI_BIAS_N_GELU, EPI_BIAS_N_RES, EPI_BIAS_M = range(4)
 
@@ -71,6 +71,9 @@ def lib() -> ctypes.CDLL:
         "kraken_weight_blob_elems": ([P(_Config)], sz),
         "kraken_load_weights": ([vp, vp, sz, ctypes.c_int, vp], i32),
         "kraken_prefill": ([vp, vp, P(i32), i32, vp, vp, vp], i32),
+        "kraken_kv_cache_bytes": ([P(_Config), i32, i32], sz),
+        "kraken_prefill_kv": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
+        "kraken_decode": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
         "kraken_destroy": ([vp], i32),
         "kraken_status_string": ([i32], ctypes.c_char_p),
         "kraken_last_error": ([], ctypes.c_char_p),
@@ -83,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "kraken_op_gemm": ([i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, i64, i64, i64,
                             vp], i32),
         "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, P(i32), i32, vp], i32),
+        "kraken_op_decode_attention": ([i32, vp, vp, vp, i32, i32, i32, P(i32), i32, i32, i32,
+                                        vp, i64, vp], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(L, name)
@@ -133,6 +138,11 @@ def torch_dtype(code: int) -> torch.dtype:
     return {DTYPE_BF16: torch.bfloat16, DTYPE_F16: torch.float16, DTYPE_F32: torch.float32}[code]
 
 
+def compute_code(cfg: "Config") -> int:
+    """dtype code of the MFMA operand type (the element type of a KV cache)."""
+    return dtype_code(cfg.dtype if cfg.compute == "storage" else cfg.compute)
+
+
 @dataclasses.dataclass
 class Config:
     n_sub: int
@@ -181,6 +191,22 @@ def pack_weights(layers: Iterable[Sequence[Mapping[str, torch.Tensor]]],
     if off != blob.numel():
         raise ValueError(f"blob has {off} elements, expected {blob.numel()}")
     return blob
+
+
+@dataclasses.dataclass
+class KVCache:
+    """Device memory of a KV cache (kraken.h layout
+    [L][N][2][max_seqs][heads][capacity][hd], compute type)."""
+    buf: torch.Tensor
+    max_seqs: int
+    capacity: int
+
+    def view(self, cfg: "Config") -> torch.Tensor:
+        """The cache as a tensor [L, N, 2, max_seqs, heads, capacity, hd]."""
+        hd = cfg.d_model // cfg.n_heads
+        dt = torch_dtype(compute_code(cfg))
+        return self.buf.view(dt).view(cfg.n_layers, cfg.n_sub, 2, self.max_seqs, cfg.n_heads,
+                                      self.capacity, hd)
 
 
 class Kraken:
@@ -236,6 +262,55 @@ class Kraken:
         cu = _cu_array(cu_seqlens)
         _check(lib().kraken_prefill(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
                                     out.data_ptr(), _ptr(sub_out), _stream(stream)))
+        return out, sub_out
+
+    # ---- KV cache and decode
+    def kv_cache_bytes(self, max_seqs: int, capacity: int) -> int:
+        return int(lib().kraken_kv_cache_bytes(ctypes.byref(self._c), max_seqs, capacity))
+
+    def new_kv_cache(self, max_seqs: int, capacity: int, device=None) -> "KVCache":
+        """Allocates (uninitialised) device memory for a cache of max_seqs slots."""
+        nbytes = self.kv_cache_bytes(max_seqs, capacity)
+        if nbytes == 0:
+            raise ValueError("invalid max_seqs or capacity")
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=device or "cuda")
+        return KVCache(buf, max_seqs, capacity)
+
+    def prefill_kv(self, hidden: torch.Tensor, cu_seqlens: Sequence[int], cache: "KVCache",
+                   out: Optional[torch.Tensor] = None, sub_out=False,
+                   stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+        """prefill() that also writes sequence b's keys and values into slot b of cache."""
+        T = int(cu_seqlens[-1])
+        out, sub_out = self._outputs(hidden, T, out, sub_out)
+        cu = _cu_array(cu_seqlens)
+        _check(lib().kraken_prefill_kv(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
+                                       out.data_ptr(), _ptr(sub_out), cache.buf.data_ptr(),
+                                       cache.max_seqs, cache.capacity, _stream(stream)))
+        return out, sub_out
+
+    def decode(self, hidden: torch.Tensor, lens: Sequence[int], cache: "KVCache",
+               out: Optional[torch.Tensor] = None, sub_out=False,
+               stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+        """One decode step: hidden [B, d] holds one new token per sequence; lens[b] is the
+        number of tokens slot b already holds.  Returns (out [B, d], sub_out [N, B, d])
+        fp32; the caller advances lens by one."""
+        B = len(lens)
+        out, sub_out = self._outputs(hidden, B, out, sub_out)
+        arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
+        _check(lib().kraken_decode(self._h, hidden.data_ptr(), arr, B, out.data_ptr(),
+                                   _ptr(sub_out), cache.buf.data_ptr(), cache.max_seqs,
+                                   cache.capacity, _stream(stream)))
+        return out, sub_out
+
+    def _outputs(self, hidden, T, out, sub_out):
+        d = self.cfg.d_model
+        if out is None:
+            out = torch.empty((T, d), dtype=torch.float32, device=hidden.device)
+        if sub_out is True:
+            sub_out = torch.empty((self.cfg.n_sub, T, d), dtype=torch.float32,
+                                  device=hidden.device)
+        elif sub_out is False:
+            sub_out = None
         return out, sub_out
 
     # ---- per-kernel timing
@@ -294,3 +369,17 @@ def op_attention(qk: torch.Tensor, vt: torch.Tensor, out: torch.Tensor, n: int, 
                                      out.data_ptr(), n, d, n_heads, cu, len(cu_seqlens) - 1,
                                      _stream(stream)))
     return out
+
+
+def op_decode_attention(qk: torch.Tensor, kv_layer: torch.Tensor, out: torch.Tensor, n: int,
+                        d: int, n_heads: int, lens: Sequence[int], max_seqs: int, capacity: int,
+                        work: torch.Tensor, stream=None) -> None:
+    """Attention of one new token per sequence over one layer of a KV cache."""
+    B = len(lens)
+    arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
+    if work.dtype != torch.float32:
+        raise ValueError("work must be float32")
+    _check(lib().kraken_op_decode_attention(dtype_code(qk.dtype), qk.data_ptr(),
+                                            kv_layer.data_ptr(), out.data_ptr(), n, d, n_heads,
+                                            arr, B, max_seqs, capacity, work.data_ptr(),
+                                            work.numel(), _stream(stream)))

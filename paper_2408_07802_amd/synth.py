@@ -33,7 +33,8 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "workload", "seq_lens", "cu_seqlens",
-           "gen_hidden", "gen_sub_layer", "gen_layer", "gen_w_concat", "torch_dtype"]
+           "gen_hidden", "gen_sub_layer", "gen_layer", "gen_w_concat", "torch_dtype",
+           "compute_dtype", "gen_cached_kv"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -74,7 +75,7 @@ BENCH_WORKLOAD = "kraken-n8-l24-d2048-h16-s8192-bf16"
 
 _TENSOR_IDS = {"hidden": 1, "ln1_g": 2, "ln1_b": 3, "Wqkv": 4, "bqkv": 5, "Wo": 6, "bo": 7,
                "ln2_g": 8, "ln2_b": 9, "W1": 10, "b1": 11, "W2": 12, "b2": 13,
-               "W_concat": 14, "lens": 15}
+               "W_concat": 14, "lens": 15, "cache_k": 16, "cache_v": 17}
 
 
 def workload(name: str) -> Workload:
@@ -161,3 +162,22 @@ def gen_w_concat(w: Workload, seed: int = 0, device="cpu") -> torch.Tensor:
     """``W_concat`` ``[N*d, d]`` ~ N(0, 0.02)."""
     return _normal((w.n_sub * w.d_model, w.d_model), _key(seed, _TENSOR_IDS["W_concat"]),
                    w.w_std, 0.0, device, torch_dtype(w))
+
+
+def compute_dtype(w: Workload) -> torch.dtype:
+    """MFMA operand type of the workload (the element type of its KV cache)."""
+    name = w.dtype if w.compute == "storage" else w.compute
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[name]
+
+
+def gen_cached_kv(w: Workload, n_tokens: int, layer: int, sub: int, seq: int, seed: int = 0,
+                  k_std: float = 1.0, v_std: float = 1.0, device="cpu"):
+    """Stand-in cached keys and values ``(K, V)``, each ``[n_tokens, d]`` ~ N(0, std^2) in
+    the compute type, for sequence ``seq`` of sub-layer ``sub`` of layer ``layer``: the
+    earlier tokens of a decode step whose prefill is not run."""
+    dt = compute_dtype(w)
+    K = _normal((n_tokens, w.d_model), _key(seed, _TENSOR_IDS["cache_k"], layer, sub, seq),
+                k_std, 0.0, device, dt)
+    V = _normal((n_tokens, w.d_model), _key(seed, _TENSOR_IDS["cache_v"], layer, sub, seq),
+                v_std, 0.0, device, dt)
+    return K, V

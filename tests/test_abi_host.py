@@ -98,3 +98,22 @@ def test_class_flops_formula():
     cu2 = [0, 3, 10]
     att = K().class_flops(cfg, K().K_ATTN, cu2)
     assert att == L * N * 4.0 * d * (3 * 4 / 2 + 7 * 8 / 2)
+
+
+def test_kv_cache_bytes():
+    # [L][N][2][max_seqs][heads][capacity][hd] elements of the compute type
+    for dtype, compute, es in [("bf16", "storage", 2), ("f32", "storage", 4), ("bf16", "f16", 2),
+                               ("bf16", "f32", 4), ("f16", "bf16", 2)]:
+        cfg = K().Config(n_sub=8, n_layers=24, d_model=2048, n_heads=16, d_ff=8192,
+                         max_tokens=8192, dtype=dtype, compute=compute)
+        c = cfg.c_struct()
+        got = K().lib().kraken_kv_cache_bytes(ctypes.byref(c), 3, 8193)
+        assert got == 24 * 8 * 2 * 3 * 8193 * 2048 * es
+    # one token of one sequence costs 2 L N d elements: N times a single-stack model of width d
+    cfg = K().Config(n_sub=4, n_layers=2, d_model=128, n_heads=4, max_tokens=4, dtype="bf16")
+    c = cfg.c_struct()
+    assert K().lib().kraken_kv_cache_bytes(ctypes.byref(c), 1, 1) == 2 * 2 * 4 * 128 * 2
+    for ms, cap in [(0, 4), (K().MAX_SEQS + 1, 4), (1, 0), (1, -3)]:
+        assert K().lib().kraken_kv_cache_bytes(ctypes.byref(c), ms, cap) == 0
+    bad = K().Config(n_sub=0, n_layers=2, d_model=128, n_heads=4, max_tokens=4).c_struct()
+    assert K().lib().kraken_kv_cache_bytes(ctypes.byref(bad), 1, 4) == 0

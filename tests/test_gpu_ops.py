@@ -242,3 +242,75 @@ def test_attention_large_logits_stay_finite():
     ref = O.causal_attention(f64(qk[0])[:, :d], f64(qk[0])[:, d:], f64(v[0]), [0, T], H)
     check_attention(f64(out[0]), ref, f64(qk[0]), np.abs(f64(v[0])), [0, T], H, "bf16",
                     "attention large logits")
+
+
+# ----------------------------------------------------------------------- decode attention
+
+DECODE_ATTN_CASES = [
+    # n, d, H, lens (cached tokens before the new one), max_seqs, capacity, work splits
+    (2, 128, 4, [0, 1, 255, 256, 257], 6, 300, None),        # hd 32, chunk edges
+    (1, 256, 4, [5000, 17, 0], 3, 5001, None),               # hd 64, 20 chunks
+    (3, 256, 2, [1023, 4096], 2, 4100, None),                 # hd 128
+    (2, 256, 2, [9000, 300, 0], 4, 9001, 2),                  # 2 chunks of 4608 keys
+    (1, 128, 1, [777], 1, 800, 1),                            # hd 128, one chunk, 4 pieces
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("case", DECODE_ATTN_CASES)
+def test_decode_attention(dtype, case):
+    n, d, H, lens, max_seqs, cap, splits = case
+    hd, B = d // H, len(lens)
+    dt = tdt(dtype)
+    g = torch.Generator(device="cpu").manual_seed(sum(lens) + 7 * d + n)
+    qk = (torch.randn((n, B, 2 * d), generator=g) * 2.0).to(dt)
+    cache = torch.full((n, 2, max_seqs, H, cap, hd), float("nan"), dtype=dt)
+    rows_k, rows_v = [], []
+    for i in range(n):
+        rk, rv = [], []
+        for b in range(B):
+            # keys and values at positions 0..lens[b]; the new token's own at lens[b]
+            k = (torch.randn((lens[b] + 1, d), generator=g) * 2.0).to(dt)
+            v = torch.randn((lens[b] + 1, d), generator=g).to(dt)
+            cache[i, 0, b, :, :lens[b] + 1] = k.view(-1, H, hd).transpose(0, 1)
+            cache[i, 1, b, :, :lens[b] + 1] = v.view(-1, H, hd).transpose(0, 1)
+            rk.append(f64(k))
+            rv.append(f64(v))
+        rows_k.append(rk)
+        rows_v.append(rv)
+    per_split = n * B * H * (hd + 2)
+    work = torch.empty(per_split * (splits or 64), dtype=torch.float32, device=DEV)
+    out = torch.full((n, B, d), float("nan"), dtype=dt, device=DEV)
+    K().op_decode_attention(qk.to(DEV), cache.to(DEV), out, n, d, H, lens, max_seqs, cap, work)
+    torch.cuda.synchronize()
+    q64 = f64(qk)
+    for i in range(n):
+        q = q64[i][:, :d]
+        k_new = np.stack([rows_k[i][b][-1] for b in range(B)])
+        v_new = np.stack([rows_v[i][b][-1] for b in range(B)])
+        K_c = [rows_k[i][b][:-1] for b in range(B)]
+        V_c = [rows_v[i][b][:-1] for b in range(B)]
+        ref = O.cached_attention(q, k_new, v_new, K_c, V_c, H)
+        wabs = O.cached_attention(q, k_new, np.abs(v_new), K_c, [np.abs(x) for x in V_c], H)
+        # fp32 scores, probabilities and accumulation; one rounding of the output to S
+        u = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 0.0}[dtype]
+        bound = u * np.abs(ref) + 2.0 ** -16 * wabs + 1e-6 * np.sqrt(np.mean(ref ** 2))
+        got = f64(out[i])
+        assert np.all(np.isfinite(got))
+        bad = np.abs(got - ref) > bound
+        assert not bad.any(), (i, int(bad.sum()), float(np.max(np.abs(got - ref) - bound)))
+
+
+def test_decode_attention_rejects_small_work_and_bad_lens():
+    n, d, H, B, cap = 1, 128, 2, 2, 8
+    qk = torch.zeros((n, B, 2 * d), dtype=torch.bfloat16, device=DEV)
+    cache = torch.zeros((n, 2, B, H, cap, d // H), dtype=torch.bfloat16, device=DEV)
+    out = torch.empty((n, B, d), dtype=torch.bfloat16, device=DEV)
+    small_work = torch.empty(n * B * H * (d // H + 2) - 1, dtype=torch.float32, device=DEV)
+    work = torch.empty(n * B * H * (d // H + 2), dtype=torch.float32, device=DEV)
+    with pytest.raises(K().KrakenError):
+        K().op_decode_attention(qk, cache, out, n, d, H, [0, 0], B, cap, small_work)
+    with pytest.raises(K().KrakenError):
+        K().op_decode_attention(qk, cache, out, n, d, H, [0, cap], B, cap, work)
+    with pytest.raises(K().KrakenError):
+        K().op_decode_attention(qk, cache, out, n, d, H, [0, 0, 0], B, cap, work)
