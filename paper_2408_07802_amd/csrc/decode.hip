@@ -22,6 +22,8 @@
 //   decode_combine_kernel merges a head's chunk partials into the attention output.
 #include <math.h>
 
+#include <algorithm>
+
 #include "kraken_internal.hpp"
 #include "../../include/kraken.h"
 
@@ -141,109 +143,145 @@ struct DecAttnParams {
   int lens[KRAKEN_MAX_SEQS];   // cached tokens of slot b, new token included at lens[b]
 };
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 template <typename S>
 __device__ __forceinline__ float to_f(S v) { return (float)v; }
 
+// Sum (max) over the lanes l ^ o for o = FROM, 2 FROM, .. < 64: lanes of one residue
+// class mod FROM.
+template <int FROM>
+__device__ __forceinline__ float xor_sum_from(float v) {
+#pragma unroll
+  for (int o = FROM; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+template <int FROM>
+__device__ __forceinline__ float xor_max_from(float v) {
+#pragma unroll
+  for (int o = FROM; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// Sum over the lanes of one aligned group of UPTO lanes.
+template <int UPTO>
+__device__ __forceinline__ float xor_sum_below(float v) {
+#pragma unroll
+  for (int o = 1; o < UPTO; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
 // Workgroup (sub-layer i, sequence b, head h, chunk s) over keys [s*chunk, (s+1)*chunk)
-// of the lens[b] + 1 keys.  Scores: thread t takes key kb + t of a 256-key piece (a dot
-// product over its key row in 16-byte loads, the query from LDS).  Values: thread t
-// accumulates two output features over every G-th key of the piece (G = 256 / (hd/2)),
-// so that each value row is read as one contiguous segment by the group.
+// of the lens[b] + 1 keys, 4 waves.  A key row of HD elements is read by LPR consecutive
+// lanes, one 16-byte chunk each, so that every load instruction of the workgroup reads
+// whole consecutive rows.  A piece of PIECE keys is R rows per lane; its keys and values
+// are loaded before any arithmetic.  Each wave keeps its own running max, sum and
+// unnormalised output (online softmax over its rows, in fp32); the four waves merge at
+// the end and write the chunk's partial (max, sum, output).
 template <typename S, int HD>
 __global__ __launch_bounds__(256) void decode_attn_kernel(DecAttnParams p) {
-  constexpr int EPC = 16 / sizeof(S);
-  constexpr int TPG = HD / 2;                 // threads per key group (two features each)
-  constexpr int G = 256 / TPG;                // key groups
-  __shared__ float qs[HD];
-  __shared__ float pw[DEC_KEYS];
-  __shared__ float red[2][4];
-  __shared__ float2 osum[G][TPG];
+  constexpr int EPC = 16 / sizeof(S);          // elements per 16-byte chunk
+  constexpr int LPR = HD / EPC;                // lanes per key row
+  constexpr int RPW = 64 / LPR;                // rows per wave per pass
+  constexpr int RPP = 4 * RPW;                 // rows per workgroup per pass
+  constexpr int R = LPR < 8 ? LPR : 8;         // passes per piece
+  constexpr int PIECE = RPP * R;
+  static_assert(DEC_KEYS % PIECE == 0, "a chunk is a whole number of pieces");
+  __shared__ float wm[4], wl[4];
+  __shared__ float wo[4][HD];
+
   int r = blockIdx.x;
   const int s = r % p.S; r /= p.S;
   const int h = r % p.H; r /= p.H;
   const int b = r % p.B;
   const int i = r / p.B;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane % LPR;                    // this lane's chunk of a row
+  const int row0 = wave * RPW + lane / LPR;    // this lane's row within a pass
   const int nkeys = p.lens[b] + 1;
   const int k_begin = s * p.chunk, k_end = min(k_begin + p.chunk, nkeys);
 
-  const S* q = static_cast<const S*>(p.qk) + ((int64_t)i * p.B + b) * 2 * p.d + h * HD;
-  if (tid < HD) qs[tid] = to_f(q[tid]) * p.scale;
-  const S* cache = static_cast<const S*>(p.cache);
-  const S* Kb = cache + cache_index(i, 0, b, h, 0, 0, p.max_seqs, p.H, p.cap, HD);
-  const S* Vb = cache + cache_index(i, 1, b, h, 0, 0, p.max_seqs, p.H, p.cap, HD);
-  __syncthreads();
-
-  float m_run = -INFINITY, l_run = 0.f, o0 = 0.f, o1 = 0.f;
-  const int g = tid / TPG, f = 2 * (tid % TPG);
-  for (int kb = k_begin; kb < k_end; kb += DEC_KEYS) {
-    const int k = kb + tid;
-    float sv = -INFINITY;
-    if (k < k_end) {
-      const S* krow = Kb + (int64_t)k * HD;
-      float acc = 0.f;
+  float q[EPC];
+  {
+    const S* qp = static_cast<const S*>(p.qk) + ((int64_t)i * p.B + b) * 2 * p.d + h * HD + c * EPC;
+    const uint4 ch = *reinterpret_cast<const uint4*>(qp);
+    const S* e = reinterpret_cast<const S*>(&ch);
 #pragma unroll
-      for (int c = 0; c < HD; c += EPC) {
-        const uint4 ch = *reinterpret_cast<const uint4*>(krow + c);
-        const S* e = reinterpret_cast<const S*>(&ch);
-#pragma unroll
-        for (int u = 0; u < EPC; ++u) acc = fmaf(to_f(e[u]), qs[c + u], acc);
-      }
-      sv = acc;
-    }
-    // piece maximum and the running rescale (block-uniform values)
-    float mx = wave_max(sv);
-    if (lane == 0) red[0][wave] = mx;
-    __syncthreads();
-    mx = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = m_run == -INFINITY ? 0.f : __expf(m_run - m_new);
-    const float pv = k < k_end ? __expf(sv - m_new) : 0.f;
-    pw[tid] = pv;
-    float ps = wave_sum(pv);
-    if (lane == 0) red[1][wave] = ps;
-    __syncthreads();
-    ps = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-    l_run = l_run * alpha + ps;
-    o0 *= alpha;
-    o1 *= alpha;
-    m_run = m_new;
-    const int nk = min(DEC_KEYS, k_end - kb);
-    for (int kk = g; kk < nk; kk += G) {
-      const float w = pw[kk];
-      const S* vrow = Vb + (int64_t)(kb + kk) * HD + f;
-      o0 = fmaf(w, to_f(vrow[0]), o0);
-      o1 = fmaf(w, to_f(vrow[1]), o1);
-    }
-    __syncthreads();    // pw and red are rewritten by the next piece
+    for (int u = 0; u < EPC; ++u) q[u] = to_f(e[u]) * p.scale;
   }
-  osum[g][tid % TPG] = make_float2(o0, o1);
+  const S* cache = static_cast<const S*>(p.cache);
+  const S* Kb = cache + cache_index(i, 0, b, h, 0, 0, p.max_seqs, p.H, p.cap, HD) + c * EPC;
+  const S* Vb = cache + cache_index(i, 1, b, h, 0, 0, p.max_seqs, p.H, p.cap, HD) + c * EPC;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  float acc[EPC];
+#pragma unroll
+  for (int u = 0; u < EPC; ++u) acc[u] = 0.f;
+
+  for (int kb = k_begin; kb < k_end; kb += PIECE) {
+    uint4 kr[R], vr[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      // rows past the chunk's end read its last row and get probability zero
+      const int k = min(kb + j * RPP + row0, k_end - 1);
+      kr[j] = *reinterpret_cast<const uint4*>(Kb + (int64_t)k * HD);
+    }
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const int k = min(kb + j * RPP + row0, k_end - 1);
+      vr[j] = *reinterpret_cast<const uint4*>(Vb + (int64_t)k * HD);
+    }
+    float sc[R];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const S* e = reinterpret_cast<const S*>(&kr[j]);
+      float a = 0.f;
+#pragma unroll
+      for (int u = 0; u < EPC; ++u) a = fmaf(to_f(e[u]), q[u], a);
+      a = xor_sum_below<LPR>(a);               // the row's full dot product, in every lane
+      sc[j] = kb + j * RPP + row0 < k_end ? a : -INFINITY;
+      mx = fmaxf(mx, sc[j]);
+    }
+    mx = xor_max_from<LPR>(mx);
+    const float m_new = fmaxf(m_run, mx);
+    const float mref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __expf(m_run - mref);
+    float ps = 0.f;
+#pragma unroll
+    for (int u = 0; u < EPC; ++u) acc[u] *= alpha;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const float pj = __expf(sc[j] - mref);
+      ps += pj;
+      const S* e = reinterpret_cast<const S*>(&vr[j]);
+#pragma unroll
+      for (int u = 0; u < EPC; ++u) acc[u] = fmaf(pj, to_f(e[u]), acc[u]);
+    }
+    l_run = l_run * alpha + ps;                // this lane's rows (repeated in LPR lanes)
+    m_run = m_new;
+  }
+
+  // wave totals: lanes of one chunk residue hold disjoint rows
+#pragma unroll
+  for (int u = 0; u < EPC; ++u) acc[u] = xor_sum_from<LPR>(acc[u]);
+  l_run = xor_sum_from<LPR>(l_run);
+  if (lane < LPR) {
+#pragma unroll
+    for (int u = 0; u < EPC; ++u) wo[wave][lane * EPC + u] = acc[u];
+  }
+  if (lane == 0) {
+    wm[wave] = m_run;
+    wl[wave] = l_run;
+  }
   __syncthreads();
   float* out = p.part + ((((int64_t)i * p.B + b) * p.H + h) * p.S + s) * (HD + 2);
-  if (tid < TPG) {
-    float a0 = 0.f, a1 = 0.f;
+  const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+  float sw[4];
 #pragma unroll
-    for (int gg = 0; gg < G; ++gg) {
-      a0 += osum[gg][tid].x;
-      a1 += osum[gg][tid].y;
-    }
-    out[2 + 2 * tid] = a0;
-    out[3 + 2 * tid] = a1;
-  }
+  for (int w = 0; w < 4; ++w) sw[w] = M == -INFINITY ? 0.f : __expf(wm[w] - M);
+  for (int f = tid; f < HD; f += 256)
+    out[2 + f] = (wo[0][f] * sw[0] + wo[1][f] * sw[1]) + (wo[2][f] * sw[2] + wo[3][f] * sw[3]);
   if (tid == 0) {
-    out[0] = m_run;
-    out[1] = l_run;
+    out[0] = M;
+    out[1] = (wl[0] * sw[0] + wl[1] * sw[1]) + (wl[2] * sw[2] + wl[3] * sw[3]);
   }
 }
 
@@ -347,12 +385,16 @@ hipError_t launch_decode_attention(DType dt, const void* qk, const void* cache_l
   const int hd = d / n_heads;
   int max_keys = 1;
   for (int b = 0; b < B; ++b) max_keys = max(max_keys, lens_host[b] + 1);
-  // splits of the key range: as many 256-key chunks as the partial buffer holds, and the
-  // chunk grows (in whole 256-key pieces) when it cannot hold one per piece
+  // Chunks of 256 .. 1024 keys (whole 256-key units) sized for about 1024 workgroups:
+  // longer chunks amortise each workgroup's query load and final merge (measured on
+  // 8192 cached keys: 1024-key chunks 15% faster than 256-key ones for one sequence,
+  // 4% for eight); the chunk grows further when the partial buffer is too small.
   const int64_t per_split = decode_partial_floats(n, B, n_heads, hd, 1);
   const int64_t max_splits = part_floats / per_split;
   if (max_splits < 1) return hipErrorInvalidValue;
-  int chunk = DEC_KEYS;
+  const int64_t triples = (int64_t)n * B * n_heads;
+  const int64_t want = ((int64_t)max_keys * triples / 1024 + DEC_KEYS - 1) / DEC_KEYS * DEC_KEYS;
+  int chunk = (int)std::min<int64_t>(std::max<int64_t>(want, DEC_KEYS), 4 * DEC_KEYS);
   while ((max_keys + chunk - 1) / chunk > max_splits) chunk += DEC_KEYS;
   DecAttnParams p;
   p.qk = qk; p.cache = cache_layer; p.part = part;

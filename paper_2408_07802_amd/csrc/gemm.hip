@@ -445,6 +445,197 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------- few rows
+//
+// GEMM for a few rows of A (M <= 64: the tokens of a decode step).  Then every weight
+// element is used at most 64 times and the kernel is bound by streaming B (the weights)
+// from HBM once, so the tiling is chosen for parallelism: a workgroup owns TW blocks of
+// 16 output columns of one batch entry and all M rows, and its 4 waves split the
+// (kgroups x K) reduction into 4 contiguous ranges, merged through LDS at the end.  Each
+// step of 32 k is one v_mfma_f32_16x16x32 per (16-row block of A, column block): lane l
+// supplies B column l % 16 and A row l % 16, k = 8 (l / 16) .. + 7 (one 16-byte load
+// each), and gets D rows 4 (l / 16) .. + 3 of column l % 16.  A rows past M load row
+// M - 1 and are masked to zero (whole 16-byte loads without branches: per-lane
+// conditional loads compile to four 4-byte loads each and halved the throughput at 8
+// rows); B columns past N load a clamped row and are not stored.
+template <typename S>
+__device__ __forceinline__ f32x4 mfma16(uint4 a, uint4 b, f32x4 c) {
+  if constexpr (__is_same(S, bf16)) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  }
+}
+
+constexpr int SK_UNROLL = 8;   // steps of 32 k whose loads are issued together
+
+// 16-byte streaming load: weights are read once per step, so they need not stay cached.
+typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream16(const void* ptr) {
+  const u32v4 v = __builtin_nontemporal_load(reinterpret_cast<const u32v4*>(ptr));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+template <typename S, int MB, int TW, int EPI>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmParams p) {
+  __shared__ float red[4][MB * TW][256];
+  using OutT = std::conditional_t<EPI == EPI_BIAS_N_RES, float, S>;
+  const int z = blockIdx.y;
+  const int n0 = blockIdx.x * 16 * TW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, kq = lane >> 4;
+  const S* Bz[TW];
+#pragma unroll
+  for (int w = 0; w < TW; ++w)
+    Bz[w] = static_cast<const S*>(p.B) + z * p.sB +
+            (int64_t)min(n0 + w * 16 + col, p.N - 1) * p.ldb + kq * 8;
+  // A rows past M load row M - 1 (whole 16-byte loads, no branches) and are masked to 0
+  const S* Az[MB];
+  uint32_t amask[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = mb * 16 + col;
+    amask[mb] = m < p.M ? 0xffffffffu : 0u;
+    Az[mb] = static_cast<const S*>(p.A) + z * p.sA + (int64_t)min(m, p.M - 1) * p.lda + kq * 8;
+  }
+  auto load_a = [&](int mb, int64_t off) {
+    uint4 v = *reinterpret_cast<const uint4*>(Az[mb] + off);
+    v.x &= amask[mb]; v.y &= amask[mb]; v.z &= amask[mb]; v.w &= amask[mb];
+    return v;
+  };
+  const int steps_per_group = p.K / 32;
+  const int steps = steps_per_group * p.kgroups;
+  const int t0 = (int)((int64_t)steps * wave / 4), t1 = (int)((int64_t)steps * (wave + 1) / 4);
+  f32x4 acc[MB * TW];
+#pragma unroll
+  for (int q = 0; q < MB * TW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // step t covers k = 32 (t mod steps_per_group) .. + 31 of group g = t / steps_per_group;
+  // (g, kk) is tracked incrementally from this wave's first step
+  int g = t0 / steps_per_group, kk = (t0 - g * steps_per_group) * 32;
+  int gb = g % p.gBmod;
+  auto advance = [&]() {
+    kk += 32;
+    if (kk == p.K) {
+      kk = 0;
+      ++g;
+      if (++gb == p.gBmod) gb = 0;
+    }
+  };
+  int t = t0;
+  for (; t + SK_UNROLL <= t1; t += SK_UNROLL) {
+    uint4 bv[SK_UNROLL][TW], av[SK_UNROLL][MB];
+    int64_t ao[SK_UNROLL], bo[SK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u) {
+      ao[u] = g * p.gA + kk;
+      bo[u] = gb * p.gB + kk;
+      advance();
+    }
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u)
+#pragma unroll
+      for (int w = 0; w < TW; ++w) bv[u][w] = load_stream16(Bz[w] + bo[u]);
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        av[u][mb] = load_a(mb, ao[u]);
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int w = 0; w < TW; ++w)
+          acc[mb * TW + w] = mfma16<S>(av[u][mb], bv[u][w], acc[mb * TW + w]);
+  }
+  for (; t < t1; ++t) {
+    uint4 bv[TW];
+#pragma unroll
+    for (int w = 0; w < TW; ++w) bv[w] = load_stream16(Bz[w] + gb * p.gB + kk);
+    const int64_t ao = g * p.gA + kk;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const uint4 av = load_a(mb, ao);
+#pragma unroll
+      for (int w = 0; w < TW; ++w) acc[mb * TW + w] = mfma16<S>(av, bv[w], acc[mb * TW + w]);
+    }
+    advance();
+  }
+  // D row 4 kq + j, column col of each 16-row block -> red[wave][mb][row * 16 + col]
+#pragma unroll
+  for (int q = 0; q < MB * TW; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red[wave][q][(kq * 4 + j) * 16 + col] = acc[q][j];
+  __syncthreads();
+  const int tid = threadIdx.x;
+  const float* biasz = p.bias ? p.bias + z * p.sBias : nullptr;
+#pragma unroll
+  for (int w = 0; w < TW; ++w) {
+    const int n = n0 + w * 16 + (tid & 15);
+    if (n >= p.N) continue;
+    const float bn = biasz ? biasz[n] : 0.f;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = mb * 16 + (tid >> 4);
+      if (m >= p.M) break;
+      const int q = mb * TW + w;
+      float v = (red[0][q][tid] + red[1][q][tid]) + (red[2][q][tid] + red[3][q][tid]) + bn;
+      if constexpr (EPI == EPI_BIAS_N_GELU) v = gelu_erf(v);
+      if constexpr (EPI == EPI_BIAS_N_RES) {
+        if (p.R) v += p.R[z * p.sR + (int64_t)m * p.ldc + n];
+      }
+      store_val<OutT>(static_cast<OutT*>(p.C) + z * p.sC + (int64_t)m * p.ldc + n, v);
+    }
+  }
+}
+
+template <typename S, int MB, int TW>
+hipError_t launch_skinny(const GemmDesc& g, hipStream_t s) {
+  GemmParams p;
+  p.A = g.A; p.B = g.B; p.C = g.C; p.bias = g.bias; p.R = g.R;
+  p.M = g.M; p.N = g.N; p.K = g.K;
+  p.lda = g.lda; p.ldb = g.ldb; p.ldc = g.ldc;
+  p.sA = g.sA; p.sB = g.sB; p.sC = g.sC; p.sR = g.sR; p.sBias = g.sBias;
+  p.kgroups = g.kgroups; p.gA = g.gA; p.gB = g.gB; p.gBmod = g.gBmod;
+  p.tiles_m = 1; p.tiles_n = (g.N + 16 * TW - 1) / (16 * TW); p.batch = g.batch;
+  dim3 grid((unsigned)p.tiles_n, (unsigned)g.batch), block(256);
+  switch (g.epi) {
+    case EPI_BIAS_N:
+      hipLaunchKernelGGL((gemm_skinny_kernel<S, MB, TW, EPI_BIAS_N>), grid, block, 0, s, p);
+      break;
+    case EPI_BIAS_N_GELU:
+      hipLaunchKernelGGL((gemm_skinny_kernel<S, MB, TW, EPI_BIAS_N_GELU>), grid, block, 0, s, p);
+      break;
+    case EPI_BIAS_N_RES:
+      hipLaunchKernelGGL((gemm_skinny_kernel<S, MB, TW, EPI_BIAS_N_RES>), grid, block, 0, s, p);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Two 16-column blocks per wave (each A fragment feeds two MFMAs, halving A loads per
+// weight byte) unless that leaves one row with fewer than 1024 workgroups, where the
+// longer per-wave reductions cost more than the A loads save (measured on the N=8,
+// d=2048 decode projections: FFN down at one row 9% slower with two blocks, every
+// projection at eight rows 10-25% faster).
+template <typename S, int MB>
+hipError_t launch_skinny_tw(const GemmDesc& g, hipStream_t s) {
+  const int64_t wgs2 = (int64_t)((g.N + 31) / 32) * g.batch;
+  if (g.M == 1 && wgs2 < 1024) return launch_skinny<S, MB, 1>(g, s);
+  return launch_skinny<S, MB, 2>(g, s);
+}
+
+template <typename S>
+hipError_t launch_skinny_rows(const GemmDesc& g, hipStream_t s) {
+  if (g.M <= 16) return launch_skinny_tw<S, 1>(g, s);
+  if (g.M <= 32) return launch_skinny_tw<S, 2>(g, s);
+  return launch_skinny_tw<S, 4>(g, s);
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmDesc& g, hipStream_t s) {
@@ -455,6 +646,11 @@ hipError_t launch_gemm(const GemmDesc& g, hipStream_t s) {
   const int64_t es = (int64_t)dtype_size(g.dt);
   if ((int64_t)g.M * g.lda * es >= (1ll << 31) || (int64_t)g.N * g.ldb * es >= (1ll << 31))
     return hipErrorInvalidValue;
+  // a few rows of 16-bit operands (a decode step): weight streaming
+  if (g.M <= 64 && g.epi != EPI_BIAS_M && g.dt != DType::F32) {
+    if (g.dt == DType::BF16) return launch_skinny_rows<bf16>(g, s);
+    return launch_skinny_rows<f16>(g, s);
+  }
   // 256 x 256 tiles when they give at least two waves of workgroups over the 256 CUs,
   // else 128 x 128 (small token counts or narrow projections).
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.batch;

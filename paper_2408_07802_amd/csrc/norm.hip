@@ -9,6 +9,8 @@
 // One workgroup owns one token: it reads the token's row of every sub-layer,
 // so each HBM byte is touched once.  Rows are read as float4, statistics are
 // kept in fp32 with a two-pass (mean, then centred variance) reduction.
+#include <algorithm>
+
 #include "kraken_internal.hpp"
 
 namespace kraken {
@@ -106,10 +108,13 @@ __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
   __shared__ float red[NORM_THREADS / 64];
   const int t = blockIdx.x;
   const int nv = my_vecs(d);
+  // sub-layers [i0, i1) of this block (gridDim.y blocks share the n sub-layers)
+  const int i0 = (int)((int64_t)n * blockIdx.y / gridDim.y);
+  const int i1 = (int)((int64_t)n * (blockIdx.y + 1) / gridDim.y);
   float4 v[MAX_VEC];
   float mean = 0.f, rstd = 0.f;
-  for (int i = 0; i < n; ++i) {
-    if (i == 0 || xs != 0) {
+  for (int i = i0; i < i1; ++i) {
+    if (i == i0 || xs != 0) {
       const float* row = x + i * xs + (int64_t)t * d;
 #pragma unroll
       for (int u = 0; u < MAX_VEC; ++u)
@@ -147,7 +152,9 @@ __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
       y[u] = a;
     }
   }
-  for (int i = 0; i < n; ++i) {
+  const int i0 = (int)((int64_t)n * blockIdx.y / gridDim.y);
+  const int i1 = (int)((int64_t)n * (blockIdx.y + 1) / gridDim.y);
+  for (int i = i0; i < i1; ++i) {
     float4 v[MAX_VEC];
     const float* hrow = h + i * plane + (int64_t)t * d;
 #pragma unroll
@@ -231,6 +238,14 @@ hipError_t by_type(DType dt, Fn&& fn) {
   return hipErrorInvalidValue;
 }
 
+// Blocks per token row: one block loops over all n sub-layers when there are enough
+// rows to fill the chip (the shared-input statistics and the N-way sum are then computed
+// once per row); few rows (a decode step) spread the sub-layers over up to n blocks.
+unsigned sub_groups(int n, int T) {
+  if (T >= 512) return 1;
+  return (unsigned)std::min(n, (512 + T - 1) / T);
+}
+
 }  // namespace
 
 hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* gamma,
@@ -240,7 +255,8 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
-    hipLaunchKernelGGL(layernorm_kernel<S>, dim3(T), dim3(NORM_THREADS), 0, s, x, xs, gamma, beta,
+    hipLaunchKernelGGL(layernorm_kernel<S>, dim3(T, sub_groups(n, T)), dim3(NORM_THREADS), 0, s,
+                       x, xs, gamma, beta,
                        static_cast<S*>(out), n, T, d, eps);
     return hipGetLastError();
   });
@@ -253,7 +269,8 @@ hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, con
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
-    hipLaunchKernelGGL(combine_ln2_kernel<S>, dim3(T), dim3(NORM_THREADS), 0, s, x, shared, h,
+    hipLaunchKernelGGL(combine_ln2_kernel<S>, dim3(T, sub_groups(n, T)), dim3(NORM_THREADS), 0, s,
+                       x, shared, h,
                        gamma, beta, static_cast<S*>(out), n, T, d, eps);
     return hipGetLastError();
   });

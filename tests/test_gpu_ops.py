@@ -99,6 +99,11 @@ GEMM_SHAPES = [  # (M, N, K, batch)
 # 16-bit operands: ragged M and N edges, and the shortest K (one 64-element slice, so the
 # double-buffered ring runs only its prologue and last slice).
 GEMM_BIG_SHAPES = [(2000, 1100, 320, 15), (1024, 1024, 64, 32)]
+# a few rows (decode steps): 16-column tiles, the reduction split over 4 waves in blocks of
+# 8 steps of 32 k plus a remainder, 1, 2 or 4 blocks of 16 rows
+GEMM_SKINNY_SHAPES = [(1, 2048, 8192, 2), (5, 1000, 2048, 3), (16, 4096, 2048, 1),
+                      (17, 33, 320, 2), (33, 130, 64, 1), (64, 2048, 1024, 2),
+                      (9, 520, 2112, 2), (3, 7, 64, 1), (1, 4096, 2048, 8)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
@@ -112,6 +117,13 @@ def test_gemm(dtype, epi, shape):
 @pytest.mark.parametrize("epi", [0, 1, 2, 3])
 @pytest.mark.parametrize("shape", GEMM_BIG_SHAPES)
 def test_gemm_big_tiles(dtype, epi, shape):
+    _check_gemm(dtype, epi, shape)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("epi", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", GEMM_SKINNY_SHAPES)
+def test_gemm_few_rows(dtype, epi, shape):
     _check_gemm(dtype, epi, shape)
 
 
