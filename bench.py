@@ -44,6 +44,15 @@ TRAFFIC = {
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
+    # decode step, one sequence of 8192 cached tokens: the attention class is the split-key
+    # kernel plus its chunk merge
+    "decode_attention_b1_ctx8192": {
+        "source": "paper_2408_07802_amd/csrc/decode.hip",
+        "source_sha256": "f257057f7424fbdb26c7ae48337e7b4c66b7e6bf64456eb67cd49804c6fccbb0",
+        "read_bytes": 538083507, "write_bytes": 659456,
+        "algorithmic_bytes": 537034752,
+        "profile": "profiles/hbm_traffic_decode_n8_l24_d2048_ctx8192.md",
+    },
 }
 METRIC = "prefill tokens/s + TTFT ms (all N sub-layers, 1 MI355X); MFMA util %"
 
@@ -99,6 +108,16 @@ def traffic_of(kernel):
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E
 
 
+def copy_probe(dev):
+    """One device copy of COPY_PROBE_BYTES: the calibration of the HBM byte counters."""
+    import torch
+    src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def decode_class_bytes(w, es, B, ctx):
     """Algorithmic HBM bytes of one decode step per kernel class: every weight matrix
     read once in the operand type (es bytes), each sequence's cached keys and values
@@ -141,6 +160,7 @@ def bench_decode(args, w, compute):
     torch.cuda.synchronize()
     del blob
     torch.cuda.empty_cache()
+    log("[bench decode] weights loaded; filling the cache")
     cache = model.new_kv_cache(B, ctx + 1)
     flat = cache.buf.view(synth.compute_dtype(w))
     g = torch.Generator(device=dev)
@@ -148,9 +168,18 @@ def bench_decode(args, w, compute):
     step = 1 << 28
     for o in range(0, flat.numel(), step):
         flat[o:o + step].normal_(generator=g)
+    torch.cuda.synchronize()
+    log(f"[bench decode] cache of {cache.buf.numel()} bytes filled")
     X = synth.gen_hidden(w, B, 0, dev)
     out = torch.empty((B, w.d_model), dtype=torch.float32, device=dev)
     lens = [ctx] * B
+    if args.pmc_probe:
+        model.decode(X, lens, cache, out=out)
+        torch.cuda.synchronize()
+        copy_probe(dev)
+        log(f"[bench decode] probe done: 1 decode step, then a {COPY_PROBE_BYTES}-byte copy")
+        model.close()
+        return
     for _ in range(args.warmup):
         model.decode(X, lens, cache, out=out)
     torch.cuda.synchronize()
@@ -211,7 +240,9 @@ def bench_decode(args, w, compute):
         "hbm_util_pct": 100.0 * total_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": dk["gbs"],
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dk["gbs"] / HBM_PEAK_GBS,
-                     "traffic": None, "avg_launch_ms": dk["avg_launch_ms"],
+                     "traffic": traffic_of(f"decode_{dominant}_b{B}_ctx{ctx}")[0],
+                     "traffic_detail": traffic_of(f"decode_{dominant}_b{B}_ctx{ctx}")[1],
+                     "avg_launch_ms": dk["avg_launch_ms"],
                      "launches_per_step": dk["launches_per_step"]},
         "kernels": kernels,
         "wall_ms_per_step": wall / args.steps * 1e3,
@@ -228,7 +259,8 @@ def main():
     ap.add_argument("--compute", default=None, help="MFMA operand type (default: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
-                    help="one prefill and one 1 GiB device copy, untimed (for HBM counters)")
+                    help="one prefill (decode step with --phase decode) and one 1 GiB "
+                         "device copy, untimed (for HBM counters)")
     ap.add_argument("--phase", choices=["prefill", "decode"], default="prefill")
     ap.add_argument("--batch", type=int, default=1, help="decode: sequences per step")
     ap.add_argument("--context", type=int, default=8192, help="decode: cached tokens each")
@@ -275,11 +307,7 @@ def main():
     if args.pmc_probe:
         model.prefill(X, cu, out=out)
         torch.cuda.synchronize()
-        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        copy_probe(dev)
         log(f"[bench] probe done: 1 prefill, then a {COPY_PROBE_BYTES}-byte device copy")
         model.close()
         return
