@@ -41,9 +41,18 @@ sub-layer, plus its own.  By causality a decode step equals the last row of the
 prefill of the extended sequence; the pins in ``tests/test_oracle_pins.py``
 check exactly that.
 
+Grouped-query attention (the Kraken paper's suggested way to shrink its larger KV
+cache, citing multi-query and grouped-query attention; appendix on the KV cache
+size): with ``n_kv_heads`` = Hkv < H key/value heads, the H query heads form Hkv
+groups of G = H / Hkv consecutive heads and every head of group g uses key/value
+head g (head h reads K/V head ``h // G``); Hkv = 1 is multi-query attention and
+Hkv = H the standard multi-head attention.  Only the key and value projections
+narrow, to dkv = Hkv * hd columns each.
+
 Weight layout taken by this module (a convention, not mathematics): every
 matrix multiplies as ``u @ W`` (row-major ``[in, out]``); ``Wqkv`` has
-columns ``[Q | K | V]`` and head ``h`` owns columns ``h*hd:(h+1)*hd`` of each.
+columns ``[Q | K | V]`` (widths d, dkv, dkv) and head ``h`` owns columns
+``h*hd:(h+1)*hd`` of Q, key/value head ``g`` columns ``g*hd:(g+1)*hd`` of K and V.
 """
 
 from __future__ import annotations
@@ -82,18 +91,22 @@ def gelu(z: np.ndarray) -> np.ndarray:
     return 0.5 * z * (1.0 + _erf(z / math.sqrt(2.0)))
 
 
-def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int) -> np.ndarray:
+def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int,
+                     n_kv_heads: int | None = None) -> np.ndarray:
     """Scaled dot-product attention with a causal mask, per head and per sequence.
 
-    Section 2.1: each head computes ``softmax(Q K^T / sqrt(hd)) V``.  ``Q, K, V``
-    are ``[T, d]`` with head ``h`` in columns ``h*hd:(h+1)*hd``; tokens of packed
-    sequence ``b`` are rows ``cu[b]:cu[b+1]`` and attend to themselves and to
-    earlier tokens of the same sequence only.  Returns the heads concatenated,
-    ``[T, d]``.
+    Section 2.1: each head computes ``softmax(Q K^T / sqrt(hd)) V``.  ``Q`` is
+    ``[T, d]`` with head ``h`` in columns ``h*hd:(h+1)*hd``; ``K, V`` are
+    ``[T, n_kv_heads*hd]`` and head ``h`` uses their head ``h // (n_heads /
+    n_kv_heads)`` (grouped-query attention; by default every head has its own).
+    Tokens of packed sequence ``b`` are rows ``cu[b]:cu[b+1]`` and attend to
+    themselves and to earlier tokens of the same sequence only.  Returns the heads
+    concatenated, ``[T, d]``.
     """
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     T, d = Q.shape
     hd = d // n_heads
+    group = n_heads // (n_kv_heads or n_heads)
     out = np.zeros((T, d), dtype=np.float64)
     for b in range(len(cu_seqlens) - 1):
         s0, s1 = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
@@ -101,29 +114,34 @@ def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int) -> np.nda
         future = np.triu(np.ones((S, S), dtype=bool), k=1)   # key index > query index
         for h in range(n_heads):
             cols = slice(h * hd, (h + 1) * hd)
-            scores = Q[s0:s1, cols] @ K[s0:s1, cols].T / math.sqrt(hd)
+            kv = slice((h // group) * hd, (h // group + 1) * hd)
+            scores = Q[s0:s1, cols] @ K[s0:s1, kv].T / math.sqrt(hd)
             scores[future] = -np.inf
             scores -= scores.max(axis=1, keepdims=True)
             p = np.exp(scores)
             p /= p.sum(axis=1, keepdims=True)
-            out[s0:s1, cols] = p @ V[s0:s1, cols]
+            out[s0:s1, cols] = p @ V[s0:s1, kv]
     return out
 
 
 def multi_head_attention(u, p: Mapping, cu_seqlens, n_heads: int,
-                         kv_out: list | None = None) -> np.ndarray:
+                         kv_out: list | None = None,
+                         n_kv_heads: int | None = None) -> np.ndarray:
     """MHA block: QKV projection, per-head causal attention, output projection.
 
+    ``Wqkv`` has ``d + 2 dkv`` columns ``[Q | K | V]``, dkv = n_kv_heads * hd.
     With ``kv_out`` (a list), appends this block's keys and values ``(K, V)``
-    (``[T, d]`` each, the projections the attention used).
+    (``[T, dkv]`` each, the projections the attention used).
     """
     u = _f64(u)
     d = u.shape[1]
+    dkv = d // n_heads * (n_kv_heads or n_heads)
     qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
-    Q, K, V = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    Q, K, V = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
     if kv_out is not None:
         kv_out.append((K, V))
-    return causal_attention(Q, K, V, cu_seqlens, n_heads) @ _f64(p["Wo"]) + _f64(p["bo"])
+    return (causal_attention(Q, K, V, cu_seqlens, n_heads, n_kv_heads) @ _f64(p["Wo"])
+            + _f64(p["bo"]))
 
 
 def feed_forward(u, p: Mapping) -> np.ndarray:
@@ -133,20 +151,22 @@ def feed_forward(u, p: Mapping) -> np.ndarray:
 
 
 def sub_layer_forward(x, y, p: Mapping, cu_seqlens, n_heads: int,
-                      eps: float = LN_EPS, kv_out: list | None = None) -> np.ndarray:
+                      eps: float = LN_EPS, kv_out: list | None = None,
+                      n_kv_heads: int | None = None) -> np.ndarray:
     """One Kraken sub-layer (Algorithm 1) given its input ``x`` and combined ``y``.
 
-    ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.  ``kv_out``: see
-    ``multi_head_attention``.
+    ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.  ``kv_out``,
+    ``n_kv_heads``: see ``multi_head_attention``.
     """
     x = _f64(x)
     h = x + multi_head_attention(layer_norm(x, p["ln1_g"], p["ln1_b"], eps),
-                                 p, cu_seqlens, n_heads, kv_out)
+                                 p, cu_seqlens, n_heads, kv_out, n_kv_heads)
     return h + feed_forward(layer_norm(h + _f64(y), p["ln2_g"], p["ln2_b"], eps), p)
 
 
 def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mapping]],
-                   W_concat, n_heads: int, eps: float = LN_EPS, return_kv: bool = False):
+                   W_concat, n_heads: int, eps: float = LN_EPS, return_kv: bool = False,
+                   n_kv_heads: int | None = None):
     """Forward pass of a stack of Kraken layers followed by ``W_concat``.
 
     ``X`` is the shared first-layer input ``[T, d]`` (Section 3.1: one set of
@@ -162,7 +182,8 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
     last layer (``[N, T, d]``) and ``out = [Y_1 | ... | Y_N] @ W_concat``
     (``[T, d]``; Section 3.1, final combine).  With ``return_kv``, also the key
     and value projections of every layer and sub-layer, ``kv[j][i] = (K, V)``
-    (``[T, d]`` each): what a decode step attends to.
+    (``[T, dkv]`` each): what a decode step attends to.  ``n_kv_heads``: key/value
+    heads per sub-layer (grouped-query attention; default ``n_heads``).
     """
     X = _f64(X)
     xs = None
@@ -178,7 +199,7 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
             y = np.sum(xs, axis=0)
         kv_j = []
         xs = [sub_layer_forward(xs[i], y, layer[i], cu_seqlens, n_heads, eps,
-                                kv_j if return_kv else None)
+                                kv_j if return_kv else None, n_kv_heads)
               for i in range(n_sub)]
         kv.append(kv_j)
     if xs is None:
@@ -190,44 +211,51 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
     return out, np.stack(xs)
 
 
-def cached_attention(q, k_new, v_new, K_cache, V_cache, n_heads: int) -> np.ndarray:
+def cached_attention(q, k_new, v_new, K_cache, V_cache, n_heads: int,
+                     n_kv_heads: int | None = None) -> np.ndarray:
     """Attention of one new token per sequence over its cached keys and its own.
 
-    ``q, k_new, v_new`` are ``[B, d]`` (row b: the new token of sequence b);
-    ``K_cache[b], V_cache[b]`` are ``[S_b, d]`` (the earlier tokens, ``S_b >= 0``).
-    Row b attends to the ``S_b + 1`` keys ``[K_cache[b]; k_new[b]]`` with the scaled
-    dot-product softmax of Section 2.1 (no mask is needed: every cached token precedes
-    the new one).  Returns ``[B, d]``, heads concatenated.
+    ``q`` is ``[B, d]`` and ``k_new, v_new`` are ``[B, dkv]`` (row b: the new token
+    of sequence b); ``K_cache[b], V_cache[b]`` are ``[S_b, dkv]`` (the earlier
+    tokens, ``S_b >= 0``).  Row b attends to the ``S_b + 1`` keys
+    ``[K_cache[b]; k_new[b]]`` with the scaled dot-product softmax of Section 2.1
+    (no mask is needed: every cached token precedes the new one); head ``h`` uses
+    key/value head ``h // (n_heads / n_kv_heads)``.  Returns ``[B, d]``, heads
+    concatenated.
     """
     q, k_new, v_new = _f64(q), _f64(k_new), _f64(v_new)
     B, d = q.shape
     hd = d // n_heads
+    group = n_heads // (n_kv_heads or n_heads)
+    dkv = k_new.shape[1]
     out = np.zeros((B, d), dtype=np.float64)
     for b in range(B):
-        Kb = np.concatenate([_f64(K_cache[b]).reshape(-1, d), k_new[b:b + 1]], axis=0)
-        Vb = np.concatenate([_f64(V_cache[b]).reshape(-1, d), v_new[b:b + 1]], axis=0)
+        Kb = np.concatenate([_f64(K_cache[b]).reshape(-1, dkv), k_new[b:b + 1]], axis=0)
+        Vb = np.concatenate([_f64(V_cache[b]).reshape(-1, dkv), v_new[b:b + 1]], axis=0)
         for h in range(n_heads):
             cols = slice(h * hd, (h + 1) * hd)
-            scores = Kb[:, cols] @ q[b, cols] / math.sqrt(hd)
+            kv = slice((h // group) * hd, (h // group + 1) * hd)
+            scores = Kb[:, kv] @ q[b, cols] / math.sqrt(hd)
             scores -= scores.max()
             p = np.exp(scores)
-            out[b, cols] = (p / p.sum()) @ Vb[:, cols]
+            out[b, cols] = (p / p.sum()) @ Vb[:, kv]
     return out
 
 
 def kraken_decode(X_new, kv_cache, layers: Iterable[Sequence[Mapping]], W_concat,
-                  n_heads: int, eps: float = LN_EPS):
+                  n_heads: int, eps: float = LN_EPS, n_kv_heads: int | None = None):
     """One decode step: the next token of each of B sequences through the stack.
 
     ``X_new`` is ``[B, d]`` (row b: the new token of sequence b; its first-layer
     input, shared by the N sub-layers as in the prefill).  ``kv_cache[j][i] =
     (K, V)`` where ``K[b], V[b]`` are the ``[S_b, d]`` keys and values of sequence
-    b's earlier tokens at layer j, sub-layer i.  Each layer runs Algorithm 1 on the
-    new rows (combine ``y`` as in the prefill: ``X_new`` at the first layer, else the
-    sum of the N previous outputs), the attention being ``cached_attention``.
+    b's earlier tokens at layer j, sub-layer i (``[S_b, dkv]`` with grouped-query
+    attention).  Each layer runs Algorithm 1 on the new rows (combine ``y`` as in the
+    prefill: ``X_new`` at the first layer, else the sum of the N previous outputs),
+    the attention being ``cached_attention``.
 
     Returns ``(out [B, d], sub_out [N, B, d], kv_new)`` with ``kv_new[j][i] = (k, v)``,
-    the new tokens' keys and values (``[B, d]`` each), which a following step appends.
+    the new tokens' keys and values (``[B, dkv]`` each), which a following step appends.
     """
     X = _f64(X_new)
     xs = None
@@ -242,12 +270,13 @@ def kraken_decode(X_new, kv_cache, layers: Iterable[Sequence[Mapping]], W_concat
             p = layer[i]
             x = xs[i]
             d = x.shape[1]
+            dkv = d // n_heads * (n_kv_heads or n_heads)
             u = layer_norm(x, p["ln1_g"], p["ln1_b"], eps)
             qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
-            q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+            q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
             kv_j.append((k, v))
             K_c, V_c = kv_cache[j][i]
-            a = cached_attention(q, k, v, K_c, V_c, n_heads)
+            a = cached_attention(q, k, v, K_c, V_c, n_heads, n_kv_heads)
             h = x + a @ _f64(p["Wo"]) + _f64(p["bo"])
             nxt.append(h + feed_forward(layer_norm(h + y, p["ln2_g"], p["ln2_b"], eps), p))
         xs = nxt
@@ -273,17 +302,21 @@ def split_kv(kv, cu_seqlens: Sequence[int]):
 
 def kraken_param_count(n_sub: int, n_layers: int, d: int, d_ff: int,
                        vocab: int = 0, biases: bool = True, layer_norms: bool = True,
-                       w_concat: bool = True, positions: int = 0) -> int:
+                       w_concat: bool = True, positions: int = 0,
+                       kv_width: int | None = None) -> int:
     """Number of parameters of a Kraken model.
 
     Per sub-layer: QKV (3d^2) + output projection (d^2) + FFN (2 d d_ff), plus
     optional biases (3d + d + d_ff + d) and two LayerNorms (4d) -- Section 3.2's
     closed form counts only the matrices.  ``W_concat`` adds N d^2 (Section 3.1),
-    token and position embeddings add ``(vocab + positions) * d``.
+    token and position embeddings add ``(vocab + positions) * d``.  With grouped-query
+    attention the key and value projections are ``kv_width`` (= n_kv_heads * hd)
+    wide instead of d: QKV is ``d (d + 2 kv_width)`` and its bias ``d + 2 kv_width``.
     """
-    per_sub = 4 * d * d + 2 * d * d_ff
+    dkv = d if kv_width is None else kv_width
+    per_sub = d * (d + 2 * dkv) + d * d + 2 * d * d_ff
     if biases:
-        per_sub += 3 * d + d + d_ff + d
+        per_sub += (d + 2 * dkv) + d + d_ff + d
     if layer_norms:
         per_sub += 4 * d
     total = n_layers * n_sub * per_sub

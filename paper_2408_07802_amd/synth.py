@@ -51,10 +51,19 @@ class Workload:
     w_std: float = 0.02
     out_proj_std: Optional[float] = None       # std of Wo and W2 (None: w_std)
     compute: str = "storage"                   # MFMA operand type the prefill runs with
+    n_kv_heads: int = 0                        # key/value heads (0: n_heads)
 
     @property
     def head_dim(self) -> int:
         return self.d_model // self.n_heads
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_kv_heads or self.n_heads
+
+    @property
+    def kv_width(self) -> int:
+        return self.kv_heads * self.head_dim
 
 
 WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
@@ -126,7 +135,7 @@ def gen_hidden(w: Workload, n_tokens: int, seed: int = 0, device="cpu") -> torch
 def gen_sub_layer(w: Workload, layer: int, sub: int, seed: int = 0, device="cpu",
                   affine: str = "plain") -> Dict[str, torch.Tensor]:
     """Parameters of sub-layer ``sub`` of layer ``layer`` (x @ W layout, [in, out])."""
-    d, f = w.d_model, w.d_ff
+    d, f, dkv = w.d_model, w.d_ff, w.kv_width
     dt = torch_dtype(w)
     ostd = w.out_proj_std if w.out_proj_std is not None else w.w_std
 
@@ -145,7 +154,7 @@ def gen_sub_layer(w: Workload, layer: int, sub: int, seed: int = 0, device="cpu"
         raise ValueError(f"unknown affine variant {affine!r}")
     return {
         "ln1_g": vec("ln1_g", d, "gamma"), "ln1_b": vec("ln1_b", d, "beta"),
-        "Wqkv": mat("Wqkv", (d, 3 * d), w.w_std), "bqkv": vec("bqkv", 3 * d, "bias"),
+        "Wqkv": mat("Wqkv", (d, d + 2 * dkv), w.w_std), "bqkv": vec("bqkv", d + 2 * dkv, "bias"),
         "Wo": mat("Wo", (d, d), ostd), "bo": vec("bo", d, "bias"),
         "ln2_g": vec("ln2_g", d, "gamma"), "ln2_b": vec("ln2_b", d, "beta"),
         "W1": mat("W1", (d, f), w.w_std), "b1": vec("b1", f, "bias"),
@@ -172,12 +181,12 @@ def compute_dtype(w: Workload) -> torch.dtype:
 
 def gen_cached_kv(w: Workload, n_tokens: int, layer: int, sub: int, seq: int, seed: int = 0,
                   k_std: float = 1.0, v_std: float = 1.0, device="cpu"):
-    """Stand-in cached keys and values ``(K, V)``, each ``[n_tokens, d]`` ~ N(0, std^2) in
+    """Stand-in cached keys and values ``(K, V)``, each ``[n_tokens, dkv]`` ~ N(0, std^2) in
     the compute type, for sequence ``seq`` of sub-layer ``sub`` of layer ``layer``: the
     earlier tokens of a decode step whose prefill is not run."""
     dt = compute_dtype(w)
-    K = _normal((n_tokens, w.d_model), _key(seed, _TENSOR_IDS["cache_k"], layer, sub, seq),
+    K = _normal((n_tokens, w.kv_width), _key(seed, _TENSOR_IDS["cache_k"], layer, sub, seq),
                 k_std, 0.0, device, dt)
-    V = _normal((n_tokens, w.d_model), _key(seed, _TENSOR_IDS["cache_v"], layer, sub, seq),
+    V = _normal((n_tokens, w.kv_width), _key(seed, _TENSOR_IDS["cache_v"], layer, sub, seq),
                 v_std, 0.0, device, dt)
     return K, V

@@ -20,20 +20,21 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 # ----------------------------------------------------------------------------- helpers
 
-def rand_params(rng, d, f, scale=0.3, affine=True):
-    """Random fp64 sub-layer parameters (x @ W layout)."""
+def rand_params(rng, d, f, scale=0.3, affine=True, dkv=None):
+    """Random fp64 sub-layer parameters (x @ W layout); K and V are dkv wide."""
+    w = d + 2 * (d if dkv is None else dkv)
     p = {
-        "Wqkv": rng.normal(0, scale, (d, 3 * d)), "Wo": rng.normal(0, scale, (d, d)),
+        "Wqkv": rng.normal(0, scale, (d, w)), "Wo": rng.normal(0, scale, (d, d)),
         "W1": rng.normal(0, scale, (d, f)), "W2": rng.normal(0, scale, (f, d)),
     }
     if affine:
         p.update(ln1_g=1 + rng.normal(0, 0.2, d), ln1_b=rng.normal(0, 0.2, d),
                  ln2_g=1 + rng.normal(0, 0.2, d), ln2_b=rng.normal(0, 0.2, d),
-                 bqkv=rng.normal(0, 0.2, 3 * d), bo=rng.normal(0, 0.2, d),
+                 bqkv=rng.normal(0, 0.2, w), bo=rng.normal(0, 0.2, d),
                  b1=rng.normal(0, 0.2, f), b2=rng.normal(0, 0.2, d))
     else:
         p.update(ln1_g=np.ones(d), ln1_b=np.zeros(d), ln2_g=np.ones(d), ln2_b=np.zeros(d),
-                 bqkv=np.zeros(3 * d), bo=np.zeros(d), b1=np.zeros(f), b2=np.zeros(d))
+                 bqkv=np.zeros(w), bo=np.zeros(d), b1=np.zeros(f), b2=np.zeros(d))
     return p
 
 
@@ -500,3 +501,135 @@ def test_cached_attention_matches_brute_force():
         V = [list(r) for r in np.vstack([Vc[b], v[b:b + 1]])]
         ref = brute_attention(Q, K, V, [0, S + 1], H)[S]
         assert rel_err(got[b], ref) < 1e-12
+
+
+# ------------------------------------------------ grouped-query and multi-query attention
+# With Hkv key/value heads, query head h of a group of G = H / Hkv consecutive heads uses
+# key/value head h // G.  That is multi-head attention whose key and value weights repeat
+# each shared head's columns for every query head of its group: the pins build that
+# multi-head model explicitly and compare whole stacks, prefill and decode.
+
+def _repeat_kv_heads(p, d, H, Hkv):
+    """Multi-head parameters equal to grouped-query ``p``: K/V head columns repeated."""
+    hd, G = d // H, H // Hkv
+    dkv = Hkv * hd
+    W, bias = p["Wqkv"], p["bqkv"]
+    q_w, k_w, v_w = W[:, :d], W[:, d:d + dkv], W[:, d + dkv:]
+    q_b, k_b, v_b = bias[:d], bias[d:d + dkv], bias[d + dkv:]
+    k_cols, v_cols, kb, vb = [], [], [], []
+    for h in range(H):
+        g = h // G                     # the shared head this query head reads
+        k_cols.append(k_w[:, g * hd:(g + 1) * hd])
+        v_cols.append(v_w[:, g * hd:(g + 1) * hd])
+        kb.append(k_b[g * hd:(g + 1) * hd])
+        vb.append(v_b[g * hd:(g + 1) * hd])
+    out = dict(p)
+    out["Wqkv"] = np.concatenate([q_w] + k_cols + v_cols, axis=1)
+    out["bqkv"] = np.concatenate([q_b] + kb + vb)
+    return out
+
+
+@pytest.mark.parametrize("H,Hkv", [(4, 2), (4, 1), (6, 3), (6, 2)])
+def test_gqa_prefill_equals_mha_with_repeated_kv_heads(H, Hkv):
+    rng = np.random.default_rng(40 + H * 10 + Hkv)
+    d, f, n_sub, n_layers = 12, 20, 2, 2
+    hd = d // H
+    layers = [[rand_params(rng, d, f, dkv=Hkv * hd) for _ in range(n_sub)]
+              for _ in range(n_layers)]
+    mha = [[_repeat_kv_heads(p, d, H, Hkv) for p in row] for row in layers]
+    wcat = rng.normal(0, 0.3, (n_sub * d, d))
+    cu = [0, 5, 6, 9]
+    X = rng.normal(0, 1, (9, d))
+    out_g, sub_g, kv_g = O.kraken_prefill(X, cu, layers, wcat, H, return_kv=True,
+                                          n_kv_heads=Hkv)
+    out_m, sub_m = O.kraken_prefill(X, cu, mha, wcat, H)
+    assert rel_err(out_g, out_m) < 1e-12 and rel_err(sub_g, sub_m) < 1e-12
+    assert kv_g[0][0][0].shape == (9, Hkv * hd)
+    # a wrong grouping (head h reading shared head h mod Hkv) would differ
+    if 1 < Hkv < H:
+        wrong = O.causal_attention(X, X[:, :Hkv * hd], X[:, :Hkv * hd], cu, H, Hkv)
+        alt = np.zeros_like(wrong)
+        for h in range(H):
+            g = h % Hkv
+            alt[:, h * hd:(h + 1) * hd] = O.causal_attention(
+                X[:, h * hd:(h + 1) * hd], X[:, g * hd:(g + 1) * hd],
+                X[:, g * hd:(g + 1) * hd], cu, 1)
+        assert rel_err(wrong, alt) > 1e-3
+
+
+def brute_mqa(Q, K, V, cu, n_heads):
+    """Multi-query attention with explicit loops: every head uses the single K/V head."""
+    T, d = len(Q), len(Q[0])
+    hd = d // n_heads
+    out = [[0.0] * d for _ in range(T)]
+    for b in range(len(cu) - 1):
+        for h in range(n_heads):
+            for t in range(cu[b], cu[b + 1]):
+                logits = []
+                for u in range(cu[b], t + 1):
+                    s = 0.0
+                    for c in range(hd):
+                        s += Q[t][h * hd + c] * K[u][c]
+                    logits.append(s / math.sqrt(hd))
+                mx = max(logits)
+                w = [math.exp(v - mx) for v in logits]
+                z = sum(w)
+                for c in range(hd):
+                    out[t][h * hd + c] = sum(w[k] / z * V[u][c]
+                                             for k, u in enumerate(range(cu[b], t + 1)))
+    return out
+
+
+def test_mqa_attention_brute_force():
+    rng = np.random.default_rng(3)
+    H, hd = 3, 2
+    cu = [0, 4, 7]
+    Q = rng.normal(0, 1, (7, H * hd))
+    K = rng.normal(0, 1, (7, hd))
+    V = rng.normal(0, 1, (7, hd))
+    got = O.causal_attention(Q, K, V, cu, H, 1)
+    ref = brute_mqa(Q.tolist(), K.tolist(), V.tolist(), cu, H)
+    assert rel_err(got, ref) < 1e-12
+
+
+@pytest.mark.parametrize("Hkv", [1, 2])
+def test_gqa_decode_equals_last_row_of_extended_prefill(Hkv):
+    rng = np.random.default_rng(17 + Hkv)
+    d, f, H, n_sub, n_layers = 8, 16, 4, 2, 2
+    layers = [[rand_params(rng, d, f, dkv=Hkv * d // H) for _ in range(n_sub)]
+              for _ in range(n_layers)]
+    wcat = rng.normal(0, 0.3, (n_sub * d, d))
+    X_full = [rng.normal(0, 1, (S + 1, d)) for S in (3, 1, 5)]
+    cu_p = [0]
+    for x in X_full:
+        cu_p.append(cu_p[-1] + len(x) - 1)
+    _, _, kv_p = O.kraken_prefill(np.concatenate([x[:-1] for x in X_full]), cu_p, layers,
+                                  wcat, H, return_kv=True, n_kv_heads=Hkv)
+    cu_e = [0]
+    for x in X_full:
+        cu_e.append(cu_e[-1] + len(x))
+    out_e, sub_e = O.kraken_prefill(np.concatenate(X_full), cu_e, layers, wcat, H,
+                                    n_kv_heads=Hkv)
+    X_new = np.stack([x[-1] for x in X_full])
+    out_d, sub_d, kv_new = O.kraken_decode(X_new, O.split_kv(kv_p, cu_p), layers, wcat, H,
+                                           n_kv_heads=Hkv)
+    last = [cu_e[b + 1] - 1 for b in range(len(X_full))]
+    assert rel_err(out_d, out_e[last]) < 1e-12
+    assert rel_err(sub_d, sub_e[:, last]) < 1e-12
+    assert kv_new[0][0][0].shape == (3, Hkv * d // H)
+    # the same step through the repeated-head multi-head model
+    mha = [[_repeat_kv_heads(p, d, H, Hkv) for p in row] for row in layers]
+    _, _, kv_m = O.kraken_prefill(np.concatenate([x[:-1] for x in X_full]), cu_p, mha, wcat,
+                                  H, return_kv=True)
+    out_m, _, _ = O.kraken_decode(X_new, O.split_kv(kv_m, cu_p), mha, wcat, H)
+    assert rel_err(out_d, out_m) < 1e-12
+
+
+def test_gqa_parameter_count():
+    # the key and value projections narrow from d to Hkv * hd columns each
+    d, f, N, L, H = 2048, 8192, 8, 24, 16
+    full = O.kraken_param_count(N, L, d, f)
+    for Hkv in (16, 4, 1):
+        dkv = Hkv * d // H
+        got = O.kraken_param_count(N, L, d, f, kv_width=dkv)
+        assert full - got == N * L * 2 * (d - dkv) * (d + 1)
