@@ -79,7 +79,7 @@ def cpu_baseline(w, T, seed=0):
     y = x * float(w.n_sub)          # any combine input: the cost does not depend on it
     cu = [0, T]
     t0 = time.perf_counter()
-    O.sub_layer_forward(x, y, p, cu, w.n_heads)
+    O.sub_layer_forward(x, y, p, cu, w.n_heads, n_kv_heads=w.kv_heads)
     dt = time.perf_counter() - t0
     stack_s = dt * w.n_sub * w.n_layers
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -123,14 +123,14 @@ def decode_class_bytes(w, es, B, ctx):
     read once in the operand type (es bytes), each sequence's cached keys and values
     of ctx + 1 positions read once, the new keys and values written once, fp32
     activations of the B rows read and written once per kernel."""
-    N, L, d, F = w.n_sub, w.n_layers, w.d_model, w.d_ff
+    N, L, d, F, dkv = w.n_sub, w.n_layers, w.d_model, w.d_ff, w.kv_width
     act = lambda cols: B * cols * 4
     return {
         "ln1": L * (act(N * d) + B * N * d * es),
-        "gemm_qk": L * N * (2 * d * d * es + B * d * es + B * 2 * d * es),
-        "gemm_vt": L * N * (d * d * es + B * d * es + B * d * es),
-        "kv_cache": L * N * B * 2 * d * es * 2,
-        "attention": L * N * (B * (ctx + 1) * 2 * d * es + B * 2 * d * es + B * d * es),
+        "gemm_qk": L * N * ((d + dkv) * d * es + B * d * es + B * (d + dkv) * es),
+        "gemm_vt": L * N * (dkv * d * es + B * d * es + B * dkv * es),
+        "kv_cache": L * N * B * 2 * dkv * es * 2,
+        "attention": L * N * (B * (ctx + 1) * 2 * dkv * es + B * (d + dkv) * es + B * d * es),
         "gemm_o": L * N * (d * d * es + B * d * es + 2 * act(d)),
         "combine_ln2": L * (2 * N * act(d) + N * B * d * es),
         "gemm_up": L * N * (F * d * es + B * d * es + B * F * es),
@@ -151,7 +151,7 @@ def bench_decode(args, w, compute):
     torch.cuda.set_device(0)
     cfg = kraken.Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
                         n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=max(B, 8192), dtype=w.dtype,
-                        compute=w.compute)
+                        compute=w.compute, n_kv_heads=w.n_kv_heads)
     log(f"[bench decode] {w.name} B={B} context={ctx} compute={compute}")
     model = kraken.Kraken(cfg)
     blob = kraken.pack_weights((synth.gen_layer(w, j, 0, dev) for j in range(w.n_layers)),
@@ -234,8 +234,9 @@ def bench_decode(args, w, compute):
         "data": "synthetic",
         "config": {"workload": w.name + "-decode", "batch": B, "context": ctx,
                    "n_sub": w.n_sub, "n_layers": w.n_layers, "d_model": w.d_model,
-                   "n_heads": w.n_heads, "d_ff": w.d_ff, "storage_dtype": w.dtype,
-                   "mfma_operands": compute, "kv_cache_bytes": cache.buf.numel()},
+                   "n_heads": w.n_heads, "n_kv_heads": w.kv_heads, "d_ff": w.d_ff,
+                   "storage_dtype": w.dtype, "mfma_operands": compute,
+                   "kv_cache_bytes": cache.buf.numel()},
         "hbm_bytes_per_step": total_bytes,
         "hbm_util_pct": 100.0 * total_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": dk["gbs"],
@@ -292,7 +293,7 @@ def main():
 
     cfg = kraken.Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
                         n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=T, dtype=w.dtype,
-                        compute=w.compute)
+                        compute=w.compute, n_kv_heads=w.n_kv_heads)
     log(f"[bench] workload {w.name} T={T} compute={compute}: generating weights on device")
     model = kraken.Kraken(cfg)
     blob = kraken.pack_weights((synth.gen_layer(w, j, 0, dev) for j in range(w.n_layers)),
@@ -380,8 +381,8 @@ def main():
         "dtype": compute,
         "data": "synthetic",
         "config": {"workload": w.name, "n_sub": w.n_sub, "n_layers": w.n_layers,
-                   "d_model": w.d_model, "n_heads": w.n_heads, "d_ff": w.d_ff,
-                   "seq_lens": lens, "tokens": T, "storage_dtype": w.dtype,
+                   "d_model": w.d_model, "n_heads": w.n_heads, "n_kv_heads": w.kv_heads,
+                   "d_ff": w.d_ff, "seq_lens": lens, "tokens": T, "storage_dtype": w.dtype,
                    "mfma_operands": compute, "accumulate": "f32"},
         "mfma_util_pct": 100.0 * total_flops / (ms_per_step * 1e-3) / (peak * 1e12),
         "phase_mfma_util_pct": {

@@ -85,6 +85,14 @@ typedef enum {
  *   dtype      a kraken_dtype: element type of the weight blob and of hidden_in
  *   compute    a kraken_compute: MFMA operand type (0 = same as dtype)
  *   ln_eps     LayerNorm epsilon; 0 means 1e-5
+ *   n_kv_heads key/value heads per sub-layer; 0 means n_heads (multi-head
+ *              attention).  Fewer is grouped-query attention, 1 multi-query
+ *              attention (the paper's suggested way to shrink the KV cache,
+ *              appendix on the KV cache size): the n_heads query heads form
+ *              n_kv_heads groups of consecutive heads, and query head h reads
+ *              key/value head h / (n_heads / n_kv_heads).  Must divide n_heads,
+ *              and n_kv_heads * hd (the key and value width dkv) must be a
+ *              multiple of 64.
  */
 typedef struct {
   int32_t n_sub;
@@ -96,6 +104,7 @@ typedef struct {
   int32_t dtype;
   int32_t compute;
   float ln_eps;
+  int32_t n_kv_heads;
 } kraken_config;
 
 typedef struct kraken_model kraken_model;
@@ -117,19 +126,22 @@ typedef struct kraken_model kraken_model;
 kraken_status kraken_create(const kraken_config* cfg, kraken_model** out);
 
 /*
- * Number of elements of the weight blob for cfg (0 for an invalid cfg):
- *   L * N * (4 d^2 + 2 d F + 9 d + F) + N d^2.
+ * Number of elements of the weight blob for cfg (0 for an invalid cfg), with
+ * dkv = n_kv_heads * hd (= d for multi-head attention):
+ *   L * N * (2 d^2 + 2 d dkv + 2 d F + 7 d + 2 dkv + F) + N d^2
+ * (L * N * (4 d^2 + 2 d F + 9 d + F) + N d^2 when dkv = d).
  */
 size_t kraken_weight_blob_elems(const kraken_config* cfg);
 
 /*
  * Loads the weights.  The blob holds elements of the model's dtype in this
  * logical order: for j in 0..L-1, for i in 0..N-1 (sub-layer i of layer j):
- *   ln1_g[d] ln1_b[d] Wqkv[d][3d] bqkv[3d] Wo[d][d] bo[d]
+ *   ln1_g[d] ln1_b[d] Wqkv[d][d + 2 dkv] bqkv[d + 2 dkv] Wo[d][d] bo[d]
  *   ln2_g[d] ln2_b[d] W1[d][F] b1[F] W2[F][d] b2[d]
  * and then W_concat[N d][d].  Matrices are row-major and multiply as x W
- * ([in][out]); Wqkv's columns are [Q | K | V] and head h owns columns
- * h*hd .. h*hd+hd-1 of each; W_concat's row block i multiplies Y_i.
+ * ([in][out]); Wqkv's columns are [Q | K | V] (widths d, dkv, dkv), query
+ * head h owns columns h*hd .. h*hd+hd-1 of Q and key/value head g columns
+ * g*hd .. g*hd+hd-1 of K and of V; W_concat's row block i multiplies Y_i.
  * blob_is_device selects whether `blob` is device or host memory.  The call
  * copies and repacks the blob into the model's own layout; the caller keeps
  * ownership and may free or reuse the blob once the stream has synchronised.
@@ -174,7 +186,7 @@ kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32
  * Cache: caller-owned device memory of kraken_kv_cache_bytes(cfg, max_seqs,
  * capacity) bytes, 16-byte aligned, elements of the MFMA operand type (the
  * compute type; the storage type when compute is KRAKEN_COMPUTE_STORAGE):
- *   [L][N][2 (K, V)][max_seqs][n_heads][capacity][hd]
+ *   [L][N][2 (K, V)][max_seqs][n_kv_heads][capacity][hd]
  * Slot b holds sequence b; position p of slot b holds the key (value) row of
  * that sequence's p-th token, projection bias included, as the attention of
  * kraken_prefill consumes it.  Positions at or above a sequence's length
@@ -299,25 +311,29 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
                              int64_t sR, void* stream);
 
 /*
- * kraken_op_attention (Section 2.1, causal MHA core; packed sequences):
- *   qk S [n][T][2d] (row t: Q then K, head h at columns h*hd of each half),
- *   vt S [n][d][ldv] (V transposed: row c is feature c over tokens), with
+ * kraken_op_attention (Section 2.1, causal MHA core; packed sequences), with
+ * n_kv_heads key/value heads (0 = n_heads; query head h reads key/value head
+ * h / (n_heads / n_kv_heads)) and dkv = n_kv_heads * hd:
+ *   qk S [n][T][d + dkv] (row t: Q then K, query head h at columns h*hd,
+ *      key head g at columns d + g*hd),
+ *   vt S [n][dkv][ldv] (V transposed: row c is feature c over tokens), with
  *      ldv = T rounded up to a multiple of 64 (KRAKEN_VT_LD(T)); the padding
  *      columns [T, ldv) must hold finite values (they meet zero probabilities),
  *   out S [n][T][d]: out = softmax(Q K^T / sqrt(hd) + causal mask) V per head.
  *   cu_seqlens is a HOST int32[num_seqs+1] array as in kraken_prefill.
  */
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
-                                  int32_t n, int32_t d, int32_t n_heads,
+                                  int32_t n, int32_t d, int32_t n_heads, int32_t n_kv_heads,
                                   const int32_t* cu_seqlens, int32_t num_seqs, void* stream);
 
 /*
  * kraken_op_decode_attention (Section 2.1, attention of one new token per
- * sequence over its KV cache; the kernels kraken_decode launches):
- *   qk       S [n][B][2d]: row b's Q half (columns 0..d-1) is the new token's
- *            query of sequence b (B = num_seqs); the K half is not read.
+ * sequence over its KV cache; the kernels kraken_decode launches), with
+ * n_kv_heads key/value heads as for kraken_op_attention:
+ *   qk       S [n][B][d + dkv]: row b's first d columns are the new token's
+ *            query of sequence b (B = num_seqs); the K columns are not read.
  *   kv_layer S, one layer of a KV cache as kraken.h lays it out,
- *            [n][2][max_seqs][n_heads][capacity][hd], holding keys and values
+ *            [n][2][max_seqs][n_kv_heads][capacity][hd], holding keys and values
  *            at positions 0 .. lens[b] of slot b (the new token's own at lens[b]).
  *   out      S [n][B][d]: softmax(q K^T / sqrt(hd)) V per head over those
  *            lens[b] + 1 positions.
@@ -330,9 +346,9 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
  */
 kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const void* kv_layer,
                                          void* out, int32_t n, int32_t d, int32_t n_heads,
-                                         const int32_t* lens, int32_t num_seqs, int32_t max_seqs,
-                                         int32_t capacity, float* work, int64_t work_floats,
-                                         void* stream);
+                                         int32_t n_kv_heads, const int32_t* lens,
+                                         int32_t num_seqs, int32_t max_seqs, int32_t capacity,
+                                         float* work, int64_t work_floats, void* stream);
 
 #ifdef __cplusplus
 }

@@ -2,9 +2,11 @@
 // softmax(Q K^T / sqrt(hd)) V; causal; packed sequences never attend across
 // each other).  All N sub-layers and all heads of a layer run in one launch.
 //
-// Layout: qk [n][T][2d] holds Q then K per token (head h at columns h*hd of
-// each half); vt [n][d][ldv] holds V transposed (feature-major), written that
-// way by the V projection so that V^T tiles are contiguous rows.
+// Layout: qk [n][T][d + dkv] holds Q then K per token (query head h at columns
+// h*hd, key head g at columns d + g*hd); vt [n][dkv][ldv] holds V transposed
+// (feature-major), written that way by the V projection so that V^T tiles are
+// contiguous rows.  With grouped-query attention (dkv = n_kv_heads * hd < d) query
+// head h reads key/value head h / group, group = n_heads / n_kv_heads.
 //
 // Formulation: a wave owns one or two 32-query MFMA blocks and computes the
 // score tile transposed, S^T = K Q^T.  In the MFMA result layout a lane
@@ -43,6 +45,7 @@ struct AttnParams {
   const void* vt;
   void* out;
   int n, T, d, n_heads, ldv, num_seqs;
+  int dkv, group;         // key/value width, query heads per key/value head
   int head_group;         // heads per XCD group of the workgroup order (0: plain order)
   float scale_log2;       // log2(e) / sqrt(hd)
   int cu[KRAKEN_MAX_SEQS + 1];
@@ -195,10 +198,11 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int wq0 = q0 + wave * QW;
 
-  const int64_t ld_qk = 2 * (int64_t)p.d;
+  const int64_t ld_qk = (int64_t)p.d + p.dkv;
   const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
-  const S* Kbase = qkz + p.d + h * HD;
-  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.d + h * HD) * p.ldv;
+  const int hkv = h / p.group;              // the key/value head this head reads
+  const S* Kbase = qkz + p.d + hkv * HD;
+  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv;
 
   // ---- Q fragments (B operand of S^T = K Q^T): lane's query, chunk 2*kc + lhalf
   uint4 qf[NQB][NQC];
@@ -524,10 +528,11 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   const int wlast = (wq0 >= q_hi) ? -1 : (min(wq0 + QW - 1, q_hi - 1) - kv_begin) / BKV;
   const int n_tiles = (q_hi - kv_begin + BKV - 1) / BKV;
 
-  const int64_t ld_qk = 2 * (int64_t)p.d;
+  const int64_t ld_qk = (int64_t)p.d + p.dkv;
   const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
-  const S* Kbase = qkz + p.d + h * HD;
-  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.d + h * HD) * p.ldv;
+  const int hkv = h / p.group;              // the key/value head this head reads
+  const S* Kbase = qkz + p.d + hkv * HD;
+  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv;
 
   uint4 qf[NQC];
   {
@@ -836,6 +841,10 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s) {
   p.n = a.n; p.T = a.T; p.d = a.d; p.n_heads = a.n_heads; p.ldv = vt_ld(a.T);
   p.num_seqs = a.num_seqs;
   const int hd = a.d / a.n_heads;
+  const int kvh = a.n_kv_heads > 0 ? a.n_kv_heads : a.n_heads;
+  if (a.n_heads % kvh != 0) return hipErrorInvalidValue;
+  p.dkv = kvh * hd;
+  p.group = a.n_heads / kvh;
   p.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
   p.tile_prefix[0] = 0;
   for (int b = 0; b <= a.num_seqs; ++b) p.cu[b] = a.cu_host[b];

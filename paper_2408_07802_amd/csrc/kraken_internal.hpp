@@ -78,13 +78,14 @@ struct GemmDesc {
 
 hipError_t launch_gemm(const GemmDesc& g, hipStream_t s);
 
-// Causal flash attention over packed sequences.
+// Causal flash attention over packed sequences; n_kv_heads key/value heads (query head
+// h reads head h / (n_heads / n_kv_heads)), dkv = n_kv_heads * hd.
 struct AttnDesc {
   DType dt;
-  const void* qk;   // [n][T][2d]   (Q | K per row)
-  const void* vt;   // [n][d][T]    (V transposed)
+  const void* qk;   // [n][T][d + dkv]   (Q | K per row)
+  const void* vt;   // [n][dkv][ldv]     (V transposed)
   void* out;        // [n][T][d]
-  int n, T, d, n_heads;
+  int n, T, d, n_heads, n_kv_heads;
   const int32_t* cu_host;  // host cu_seqlens [num_seqs + 1]
   int num_seqs;
 };
@@ -121,27 +122,29 @@ hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, 
 hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
                             int64_t dst_ld, int R, int C, int* overflow, hipStream_t s);
 
-// KV cache of one layer: [n][2 (K, V)][max_seqs][n_heads][capacity][hd], compute type.
-// Prefill: K from the K half of qk [n][T][2d], V from vt [n][d][vt_ld(T)]; token t of
-// sequence b (cu_host[b] <= t < cu_host[b+1]) goes to position t - cu_host[b] of slot b.
+// KV cache of one layer: [n][2 (K, V)][max_seqs][n_kv_heads][capacity][hd], compute
+// type; dkv = n_kv_heads * hd.  Prefill: K from columns d .. d+dkv-1 of qk [n][T][d + dkv],
+// V from vt [n][dkv][vt_ld(T)]; token t of sequence b (cu_host[b] <= t < cu_host[b+1])
+// goes to position t - cu_host[b] of slot b.
 hipError_t launch_kv_store(DType dt, const void* qk, const void* vt, void* cache_layer, int n,
-                           int T, int d, int n_heads, const int32_t* cu_host, int num_seqs,
-                           int max_seqs, int capacity, hipStream_t s);
+                           int T, int d, int n_heads, int n_kv_heads, const int32_t* cu_host,
+                           int num_seqs, int max_seqs, int capacity, hipStream_t s);
 
-// Decode: the K half of qk [n][B][2d] and v [n][B][d] at position lens_host[b] of slot b.
+// Decode: the K columns of qk [n][B][d + dkv] and v [n][B][dkv] at position lens_host[b]
+// of slot b.
 hipError_t launch_kv_append(DType dt, const void* qk, const void* v, void* cache_layer, int n,
-                            int B, int d, int n_heads, const int32_t* lens_host, int max_seqs,
-                            int capacity, hipStream_t s);
+                            int B, int d, int n_heads, int n_kv_heads, const int32_t* lens_host,
+                            int max_seqs, int capacity, hipStream_t s);
 
 // fp32 elements of the decode-attention partials for `splits` key chunks.
 int64_t decode_partial_floats(int n, int B, int n_heads, int hd, int splits);
 
-// out [n][B][d] = attention of the Q half of qk [n][B][2d] over keys 0..lens_host[b] of
-// slot b (the new token's own included, already appended).  part: fp32 scratch of
-// part_floats elements; the key range is split into as many chunks as it holds.
+// out [n][B][d] = attention of the Q columns of qk [n][B][d + dkv] over keys
+// 0..lens_host[b] of slot b (the new token's own included, already appended).  part: fp32
+// scratch of part_floats elements; the key range is split into as many chunks as it holds.
 hipError_t launch_decode_attention(DType dt, const void* qk, const void* cache_layer,
                                    float* part, int64_t part_floats, void* out, int n, int B,
-                                   int d, int n_heads, const int32_t* lens_host, int max_seqs,
-                                   int capacity, hipStream_t s);
+                                   int d, int n_heads, int n_kv_heads, const int32_t* lens_host,
+                                   int max_seqs, int capacity, hipStream_t s);
 
 }  // namespace kraken

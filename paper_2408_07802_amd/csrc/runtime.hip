@@ -43,11 +43,13 @@ kraken_status hip_fail(hipError_t e, const char* what) {
 
 struct LayerW {
   float *ln1_g, *ln1_b, *ln2_g, *ln2_b;  // [N][d]
-  float *bqk;                            // [N][2d]
-  float *bv, *bo, *b2;                   // [N][d]
+  float *bqk;                            // [N][d + dkv]
+  float *bv;                             // [N][dkv]
+  float *bo, *b2;                        // [N][d]
   float *b1;                             // [N][F]
-  void *WqkT;                            // [N][2d][d]
-  void *WvT, *WoT;                       // [N][d][d]
+  void *WqkT;                            // [N][d + dkv][d]
+  void *WvT;                             // [N][dkv][d]
+  void *WoT;                             // [N][d][d]
   void *W1T;                             // [N][F][d]
   void *W2T;                             // [N][d][F]
 };
@@ -60,12 +62,12 @@ struct ProfRec {
 // Element counts of the logical blob of one sub-layer, in blob order.
 struct SubOffsets {
   int64_t ln1_g, ln1_b, Wqkv, bqkv, Wo, bo, ln2_g, ln2_b, W1, b1, W2, b2, total;
-  SubOffsets(int64_t d, int64_t F) {
+  SubOffsets(int64_t d, int64_t F, int64_t dkv) {
     int64_t o = 0;
     ln1_g = o; o += d;
     ln1_b = o; o += d;
-    Wqkv = o; o += d * 3 * d;
-    bqkv = o; o += 3 * d;
+    Wqkv = o; o += d * (d + 2 * dkv);
+    bqkv = o; o += d + 2 * dkv;
     Wo = o; o += d * d;
     bo = o; o += d;
     ln2_g = o; o += d;
@@ -85,6 +87,7 @@ struct kraken_model {
   DType st;   // storage type of the blob and of hidden_in
   DType dt;   // MFMA operand type
   int N, L, d, H, F, Tmax, device;
+  int Hkv, dkv;   // key/value heads and width (grouped-query attention: Hkv < H)
   float eps;
   bool loaded = false;
   void* wmem = nullptr;
@@ -145,6 +148,13 @@ kraken_status validate_cfg(const kraken_config* c) {
   const int F = c->d_ff ? c->d_ff : 4 * c->d_model;
   if (c->d_model % 64 != 0 || F % 64 != 0)
     return fail(KRAKEN_ERR_UNSUPPORTED, "d_model and d_ff must be multiples of 64");
+  if (c->n_kv_heads < 0) return fail(KRAKEN_ERR_INVALID_ARG, "negative n_kv_heads");
+  if (c->n_kv_heads > 0) {
+    if (c->n_heads % c->n_kv_heads != 0)
+      return fail(KRAKEN_ERR_INVALID_ARG, "n_kv_heads does not divide n_heads");
+    if ((c->n_kv_heads * hd) % 64 != 0)
+      return fail(KRAKEN_ERR_UNSUPPORTED, "n_kv_heads * head size must be a multiple of 64");
+  }
   if (c->d_model > 8192) return fail(KRAKEN_ERR_UNSUPPORTED, "d_model above 8192");
   if (c->max_tokens > (1 << 22)) return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens above 4194304");
   // GEMM operands of one sub-layer are addressed with 32-bit byte offsets
@@ -205,7 +215,7 @@ struct Carver {
 // Lays out (or, with a null base, measures) the weight arena.
 size_t carve_weights(kraken_model* m, void* base) {
   Carver c(base);
-  const size_t N = m->N, d = m->d, F = m->F, es = sz(m->dt);
+  const size_t N = m->N, d = m->d, F = m->F, dkv = m->dkv, es = sz(m->dt);
   m->layers.resize(m->L);
   for (int j = 0; j < m->L; ++j) {
     LayerW& w = m->layers[j];
@@ -213,13 +223,13 @@ size_t carve_weights(kraken_model* m, void* base) {
     w.ln1_b = (float*)c.take(N * d * 4);
     w.ln2_g = (float*)c.take(N * d * 4);
     w.ln2_b = (float*)c.take(N * d * 4);
-    w.bqk = (float*)c.take(N * 2 * d * 4);
-    w.bv = (float*)c.take(N * d * 4);
+    w.bqk = (float*)c.take(N * (d + dkv) * 4);
+    w.bv = (float*)c.take(N * dkv * 4);
     w.bo = (float*)c.take(N * d * 4);
     w.b1 = (float*)c.take(N * F * 4);
     w.b2 = (float*)c.take(N * d * 4);
-    w.WqkT = c.take(N * 2 * d * d * es);
-    w.WvT = c.take(N * d * d * es);
+    w.WqkT = c.take(N * (d + dkv) * d * es);
+    w.WvT = c.take(N * dkv * d * es);
     w.WoT = c.take(N * d * d * es);
     w.W1T = c.take(N * F * d * es);
     w.W2T = c.take(N * d * F * es);
@@ -231,15 +241,15 @@ size_t carve_weights(kraken_model* m, void* base) {
 
 size_t carve_workspace(kraken_model* m, void* base) {
   Carver c(base);
-  const size_t N = m->N, d = m->d, F = m->F, T = m->Tmax, es = sz(m->dt);
+  const size_t N = m->N, d = m->d, F = m->F, T = m->Tmax, dkv = m->dkv, es = sz(m->dt);
   m->X32 = (float*)c.take(T * d * 4);
   m->xbuf = (float*)c.take(N * T * d * 4);
   m->hbuf = (float*)c.take(N * T * d * 4);
   m->act = c.take(N * T * d * es);
-  m->qk = c.take(N * T * 2 * d * es);
+  m->qk = c.take(N * T * (d + dkv) * es);
   m->o = c.take(N * T * d * es);
   // vt and g stay adjacent and last: a decode step keeps its attention partials there
-  m->vt = c.take(N * d * (size_t)vt_ld(m->Tmax) * es);
+  m->vt = c.take(N * dkv * (size_t)vt_ld(m->Tmax) * es);
   m->g = c.take(std::max(N * T * F, 2 * N * T * d) * es);
   m->ws_end = base ? static_cast<char*>(base) + c.off : nullptr;
   return c.off;
@@ -251,8 +261,8 @@ inline const char* cptr(const void* p, int64_t elems, DType t) {
 
 // Repack one sub-layer's logical parameters (device pointer `src`) into the model layout.
 hipError_t repack_sub(kraken_model* m, int j, int i, const void* src, hipStream_t s) {
-  const int64_t d = m->d, F = m->F;
-  const SubOffsets so(d, F);
+  const int64_t d = m->d, F = m->F, dkv = m->dkv, wq = d + 2 * dkv;   // Wqkv row width
+  const SubOffsets so(d, F, dkv);
   const LayerW& w = m->layers[j];
   const DType st = m->st, dt = m->dt;
   const size_t es = sz(dt);
@@ -263,17 +273,17 @@ hipError_t repack_sub(kraken_model* m, int j, int i, const void* src, hipStream_
   R_(launch_to_f32(st, cptr(src, so.ln1_b, st), w.ln1_b + i * d, d, s));
   R_(launch_to_f32(st, cptr(src, so.ln2_g, st), w.ln2_g + i * d, d, s));
   R_(launch_to_f32(st, cptr(src, so.ln2_b, st), w.ln2_b + i * d, d, s));
-  R_(launch_to_f32(st, cptr(src, so.bqkv, st), w.bqk + i * 2 * d, 2 * d, s));
-  R_(launch_to_f32(st, cptr(src, so.bqkv + 2 * d, st), w.bv + i * d, d, s));
+  R_(launch_to_f32(st, cptr(src, so.bqkv, st), w.bqk + i * (d + dkv), d + dkv, s));
+  R_(launch_to_f32(st, cptr(src, so.bqkv + d + dkv, st), w.bv + i * dkv, dkv, s));
   R_(launch_to_f32(st, cptr(src, so.bo, st), w.bo + i * d, d, s));
   R_(launch_to_f32(st, cptr(src, so.b1, st), w.b1 + i * F, F, s));
   R_(launch_to_f32(st, cptr(src, so.b2, st), w.b2 + i * d, d, s));
   // x W layout [in][out] -> [out][in], converted to the operand type
-  R_(launch_transpose(st, cptr(src, so.Wqkv, st), 3 * d, dt,
-                      static_cast<char*>(w.WqkT) + i * 2 * d * d * es, d, (int)d, (int)(2 * d),
-                      of, s));
-  R_(launch_transpose(st, cptr(src, so.Wqkv + 2 * d, st), 3 * d, dt,
-                      static_cast<char*>(w.WvT) + i * d * d * es, d, (int)d, (int)d, of, s));
+  R_(launch_transpose(st, cptr(src, so.Wqkv, st), wq, dt,
+                      static_cast<char*>(w.WqkT) + i * (d + dkv) * d * es, d, (int)d,
+                      (int)(d + dkv), of, s));
+  R_(launch_transpose(st, cptr(src, so.Wqkv + d + dkv, st), wq, dt,
+                      static_cast<char*>(w.WvT) + i * dkv * d * es, d, (int)d, (int)dkv, of, s));
   R_(launch_transpose(st, cptr(src, so.Wo, st), d, dt, static_cast<char*>(w.WoT) + i * d * d * es,
                       d, (int)d, (int)d, of, s));
   R_(launch_transpose(st, cptr(src, so.W1, st), F, dt, static_cast<char*>(w.W1T) + i * F * d * es,
@@ -304,7 +314,7 @@ struct KvRef {
 };
 
 size_t kv_layer_bytes(const kraken_model* m, int max_seqs, int cap) {
-  return (size_t)m->N * 2 * (size_t)max_seqs * (size_t)cap * (size_t)m->d * sz(m->dt);
+  return (size_t)m->N * 2 * (size_t)max_seqs * (size_t)cap * (size_t)m->dkv * sz(m->dt);
 }
 
 // fp32 elements available to a decode step's attention partials: the vt and g regions.
@@ -339,8 +349,9 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
 
   // Attention reads V^T in 16-byte chunks of 8 tokens; the padding columns [T, ldv) are
   // only ever multiplied by zero probabilities but must hold finite values.
+  const int64_t dkv = m->dkv, dqk = d + dkv;   // key/value width, Q|K row width
   if (!decode && ldv > T)
-    RUN(KRAKEN_K_OTHER, launch_zero_cols(dt, m->vt, N * d, ldv, T, ldv, s), "V padding");
+    RUN(KRAKEN_K_OTHER, launch_zero_cols(dt, m->vt, N * dkv, ldv, T, ldv, s), "V padding");
 
   for (int j = 0; j < m->L; ++j) {
     const LayerW& w = m->layers[j];
@@ -354,54 +365,54 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
       GemmDesc g = gemm_base(dt);
       g.epi = EPI_BIAS_N;
       g.A = m->act; g.lda = (int)d; g.sA = Td;
-      g.B = w.WqkT; g.ldb = (int)d; g.sB = 2 * d * d;
-      g.C = m->qk; g.ldc = (int)(2 * d); g.sC = 2 * Td;
-      g.bias = w.bqk; g.sBias = 2 * d;
-      g.M = T; g.N = (int)(2 * d); g.K = (int)d; g.batch = (int)N;
+      g.B = w.WqkT; g.ldb = (int)d; g.sB = dqk * d;
+      g.C = m->qk; g.ldc = (int)dqk; g.sC = (int64_t)T * dqk;
+      g.bias = w.bqk; g.sBias = dqk;
+      g.M = T; g.N = (int)dqk; g.K = (int)d; g.batch = (int)N;
       RUN(KRAKEN_K_GEMM_QK, launch_gemm(g, s), "QK projection");
     }
     if (!decode) {
       {
         GemmDesc g = gemm_base(dt);
         g.epi = EPI_BIAS_M;
-        g.A = w.WvT; g.lda = (int)d; g.sA = d * d;
+        g.A = w.WvT; g.lda = (int)d; g.sA = dkv * d;
         g.B = m->act; g.ldb = (int)d; g.sB = Td;
-        g.C = m->vt; g.ldc = ldv; g.sC = d * ldv;
-        g.bias = w.bv; g.sBias = d;
-        g.M = (int)d; g.N = T; g.K = (int)d; g.batch = (int)N;
+        g.C = m->vt; g.ldc = ldv; g.sC = dkv * ldv;
+        g.bias = w.bv; g.sBias = dkv;
+        g.M = (int)dkv; g.N = T; g.K = (int)d; g.batch = (int)N;
         RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
       }
       if (kv)
         RUN(KRAKEN_K_KV,
-            launch_kv_store(dt, m->qk, m->vt, cache_j, (int)N, T, (int)d, m->H, cu, num_seqs,
-                            kv->max_seqs, kv->cap, s),
+            launch_kv_store(dt, m->qk, m->vt, cache_j, (int)N, T, (int)d, m->H, m->Hkv, cu,
+                            num_seqs, kv->max_seqs, kv->cap, s),
             "KV store");
       AttnDesc a;
       a.dt = dt; a.qk = m->qk; a.vt = m->vt; a.out = m->o;
-      a.n = (int)N; a.T = T; a.d = (int)d; a.n_heads = m->H;
+      a.n = (int)N; a.T = T; a.d = (int)d; a.n_heads = m->H; a.n_kv_heads = m->Hkv;
       a.cu_host = cu; a.num_seqs = num_seqs;
       RUN(KRAKEN_K_ATTN, launch_attention(a, s), "attention");
     } else {
-      // V rows of the new tokens go through o ([N][T][d]) into the cache; o then takes
+      // V rows of the new tokens go through o ([N][T][dkv]) into the cache; o then takes
       // the attention output, after the append has read it (stream order).
       {
         GemmDesc g = gemm_base(dt);
         g.epi = EPI_BIAS_N;
         g.A = m->act; g.lda = (int)d; g.sA = Td;
-        g.B = w.WvT; g.ldb = (int)d; g.sB = d * d;
-        g.C = m->o; g.ldc = (int)d; g.sC = Td;
-        g.bias = w.bv; g.sBias = d;
-        g.M = T; g.N = (int)d; g.K = (int)d; g.batch = (int)N;
+        g.B = w.WvT; g.ldb = (int)d; g.sB = dkv * d;
+        g.C = m->o; g.ldc = (int)dkv; g.sC = (int64_t)T * dkv;
+        g.bias = w.bv; g.sBias = dkv;
+        g.M = T; g.N = (int)dkv; g.K = (int)d; g.batch = (int)N;
         RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
       }
       RUN(KRAKEN_K_KV,
-          launch_kv_append(dt, m->qk, m->o, cache_j, (int)N, T, (int)d, m->H, kv->lens,
+          launch_kv_append(dt, m->qk, m->o, cache_j, (int)N, T, (int)d, m->H, m->Hkv, kv->lens,
                            kv->max_seqs, kv->cap, s),
           "KV append");
       RUN(KRAKEN_K_ATTN,
           launch_decode_attention(dt, m->qk, cache_j, static_cast<float*>(m->vt),
                                   decode_partial_room(m), m->o, (int)N, T, (int)d, m->H,
-                                  kv->lens, kv->max_seqs, kv->cap, s),
+                                  m->Hkv, kv->lens, kv->max_seqs, kv->cap, s),
           "decode attention");
     }
     {
@@ -503,10 +514,14 @@ const char* kraken_status_string(kraken_status s) {
 const char* kraken_last_error(void) { return g_last_error.c_str(); }
 
 size_t kraken_weight_blob_elems(const kraken_config* c) {
-  if (!c || c->n_sub < 1 || c->n_layers < 1 || c->d_model < 1 || c->d_ff < 0) return 0;
+  if (!c || c->n_sub < 1 || c->n_layers < 1 || c->d_model < 1 || c->d_ff < 0 ||
+      c->n_heads < 1 || c->n_kv_heads < 0)
+    return 0;
   const uint64_t N = c->n_sub, L = c->n_layers, d = c->d_model;
   const uint64_t F = c->d_ff ? c->d_ff : 4 * d;
-  return (size_t)(L * N * (4 * d * d + 2 * d * F + 9 * d + F) + N * d * d);
+  const uint64_t dkv = c->n_kv_heads ? (uint64_t)c->n_kv_heads * (d / c->n_heads) : d;
+  return (size_t)(L * N * (2 * d * d + 2 * d * dkv + 2 * d * F + 7 * d + 2 * dkv + F) +
+                  N * d * d);
 }
 
 kraken_status kraken_create(const kraken_config* cfg, kraken_model** out) {
@@ -523,6 +538,8 @@ kraken_status kraken_create(const kraken_config* cfg, kraken_model** out) {
   m->L = cfg->n_layers;
   m->d = cfg->d_model;
   m->H = cfg->n_heads;
+  m->Hkv = cfg->n_kv_heads > 0 ? cfg->n_kv_heads : cfg->n_heads;
+  m->dkv = m->Hkv * (cfg->d_model / cfg->n_heads);
   m->F = cfg->d_ff ? cfg->d_ff : 4 * cfg->d_model;
   m->Tmax = cfg->max_tokens;
   m->eps = cfg->ln_eps > 0.f ? cfg->ln_eps : 1e-5f;
@@ -576,7 +593,7 @@ kraken_status kraken_load_weights(kraken_model* m, const void* blob, size_t nbyt
   if (st != KRAKEN_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t d = m->d, N = m->N;
-  const SubOffsets so(d, m->F);
+  const SubOffsets so(d, m->F, m->dkv);
   const int64_t layer_elems = N * so.total;
   const int64_t wcat_off = (int64_t)m->L * layer_elems;
   void* staging = nullptr;
@@ -658,8 +675,10 @@ size_t kraken_kv_cache_bytes(const kraken_config* c, int32_t max_seqs, int32_t c
   if (max_seqs < 1 || max_seqs > KRAKEN_MAX_SEQS || capacity < 1) return 0;
   const DType st = (DType)c->dtype;
   const DType dt = c->compute == KRAKEN_COMPUTE_STORAGE ? st : (DType)(c->compute - 1);
+  const size_t dkv = c->n_kv_heads > 0 ? (size_t)c->n_kv_heads * (c->d_model / c->n_heads)
+                                        : (size_t)c->d_model;
   return (size_t)c->n_layers * (size_t)c->n_sub * 2 * (size_t)max_seqs * (size_t)capacity *
-         (size_t)c->d_model * sz(dt);
+         dkv * sz(dt);
 }
 
 kraken_status kraken_prefill_kv(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
@@ -786,9 +805,11 @@ double kraken_class_flops(const kraken_config* c, int cls, const int32_t* cu, in
   const double N = c->n_sub, L = c->n_layers, d = c->d_model;
   const double F = c->d_ff ? c->d_ff : 4.0 * d;
   const double T = cu[num_seqs];
+  const double dkv =
+      (c->n_kv_heads > 0 && c->n_heads > 0) ? (double)c->n_kv_heads * (c->d_model / c->n_heads) : d;
   switch (cls) {
-    case KRAKEN_K_GEMM_QK: return L * N * 2.0 * T * d * 2.0 * d;
-    case KRAKEN_K_GEMM_VT: return L * N * 2.0 * T * d * d;
+    case KRAKEN_K_GEMM_QK: return L * N * 2.0 * T * d * (d + dkv);
+    case KRAKEN_K_GEMM_VT: return L * N * 2.0 * T * d * dkv;
     case KRAKEN_K_GEMM_O: return L * N * 2.0 * T * d * d;
     case KRAKEN_K_GEMM_UP: return L * N * 2.0 * T * d * F;
     case KRAKEN_K_GEMM_DOWN: return L * N * 2.0 * T * F * d;
@@ -858,8 +879,8 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
 }
 
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
-                                  int32_t n, int32_t d, int32_t n_heads, const int32_t* cu_seqlens,
-                                  int32_t num_seqs, void* stream) {
+                                  int32_t n, int32_t d, int32_t n_heads, int32_t n_kv_heads,
+                                  const int32_t* cu_seqlens, int32_t num_seqs, void* stream) {
   if (!qk || !vt || !out) return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
   if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
@@ -867,12 +888,14 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
   const int hd = d / n_heads;
   if (hd != 32 && hd != 64 && hd != 128) return fail(KRAKEN_ERR_UNSUPPORTED, "head size");
+  if (n_kv_heads < 0 || (n_kv_heads > 0 && n_heads % n_kv_heads != 0))
+    return fail(KRAKEN_ERR_INVALID_ARG, "n_kv_heads must be 0 or divide n_heads");
   int64_t T = 0;
   kraken_status st = check_cu(cu_seqlens, num_seqs, INT32_MAX, &T);
   if (st != KRAKEN_OK) return st;
   AttnDesc a;
   a.dt = (DType)dtype; a.qk = qk; a.vt = vt; a.out = out;
-  a.n = n; a.T = (int)T; a.d = d; a.n_heads = n_heads;
+  a.n = n; a.T = (int)T; a.d = d; a.n_heads = n_heads; a.n_kv_heads = n_kv_heads;
   a.cu_host = cu_seqlens; a.num_seqs = num_seqs;
   hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "attention");
@@ -880,9 +903,9 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
 
 kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const void* kv_layer,
                                          void* out, int32_t n, int32_t d, int32_t n_heads,
-                                         const int32_t* lens, int32_t num_seqs, int32_t max_seqs,
-                                         int32_t capacity, float* work, int64_t work_floats,
-                                         void* stream) {
+                                         int32_t n_kv_heads, const int32_t* lens,
+                                         int32_t num_seqs, int32_t max_seqs, int32_t capacity,
+                                         float* work, int64_t work_floats, void* stream) {
   if (!qk || !kv_layer || !out || !lens || !work)
     return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
   if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
@@ -891,6 +914,8 @@ kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const vo
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
   const int hd = d / n_heads;
   if (hd != 32 && hd != 64 && hd != 128) return fail(KRAKEN_ERR_UNSUPPORTED, "head size");
+  if (n_kv_heads < 0 || (n_kv_heads > 0 && n_heads % n_kv_heads != 0))
+    return fail(KRAKEN_ERR_INVALID_ARG, "n_kv_heads must be 0 or divide n_heads");
   if (num_seqs < 1 || num_seqs > KRAKEN_MAX_SEQS || max_seqs < num_seqs ||
       max_seqs > KRAKEN_MAX_SEQS || capacity < 1)
     return fail(KRAKEN_ERR_INVALID_ARG, "num_seqs, max_seqs or capacity out of range");
@@ -902,8 +927,8 @@ kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const vo
   if (work_floats < decode_partial_floats(n, num_seqs, n_heads, hd, 1))
     return fail(KRAKEN_ERR_INVALID_ARG, "work is smaller than n * B * n_heads * (hd + 2)");
   hipError_t e = launch_decode_attention((DType)dtype, qk, kv_layer, work, work_floats, out, n,
-                                         num_seqs, d, n_heads, lens, max_seqs, capacity,
-                                         static_cast<hipStream_t>(stream));
+                                         num_seqs, d, n_heads, n_kv_heads, lens, max_seqs,
+                                         capacity, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "decode attention");
 }
 

@@ -48,7 +48,7 @@ class _Config(ctypes.Structure):
                 ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("d_ff", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float)]
+                ("ln_eps", ctypes.c_float), ("n_kv_heads", ctypes.c_int32)]
 
 
 _lib = None
@@ -85,9 +85,9 @@ def lib() -> ctypes.CDLL:
         "kraken_op_combine_ln2": ([i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, fp, vp], i32),
         "kraken_op_gemm": ([i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, i64, i64, i64,
                             vp], i32),
-        "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, P(i32), i32, vp], i32),
-        "kraken_op_decode_attention": ([i32, vp, vp, vp, i32, i32, i32, P(i32), i32, i32, i32,
-                                        vp, i64, vp], i32),
+        "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32), i32, vp], i32),
+        "kraken_op_decode_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32), i32, i32,
+                                        i32, vp, i64, vp], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(L, name)
@@ -154,11 +154,16 @@ class Config:
     dtype: str = "bf16"          # storage type of the weight blob and the input
     compute: str = "storage"     # MFMA operand type: "storage", "f32", "bf16" or "f16"
     ln_eps: float = 0.0
+    n_kv_heads: int = 0          # key/value heads (0: n_heads; fewer: grouped-query)
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_kv_heads or self.n_heads
 
     def c_struct(self) -> _Config:
         return _Config(self.n_sub, self.n_layers, self.d_model, self.n_heads, self.d_ff,
                        self.max_tokens, dtype_code(self.dtype), COMPUTE_CODES[self.compute],
-                       self.ln_eps)
+                       self.ln_eps, self.n_kv_heads)
 
 
 def weight_blob_elems(cfg: Config) -> int:
@@ -202,10 +207,10 @@ class KVCache:
     capacity: int
 
     def view(self, cfg: "Config") -> torch.Tensor:
-        """The cache as a tensor [L, N, 2, max_seqs, heads, capacity, hd]."""
+        """The cache as a tensor [L, N, 2, max_seqs, kv_heads, capacity, hd]."""
         hd = cfg.d_model // cfg.n_heads
         dt = torch_dtype(compute_code(cfg))
-        return self.buf.view(dt).view(cfg.n_layers, cfg.n_sub, 2, self.max_seqs, cfg.n_heads,
+        return self.buf.view(dt).view(cfg.n_layers, cfg.n_sub, 2, self.max_seqs, cfg.kv_heads,
                                       self.capacity, hd)
 
 
@@ -363,17 +368,18 @@ def vt_ld(T: int) -> int:
 
 
 def op_attention(qk: torch.Tensor, vt: torch.Tensor, out: torch.Tensor, n: int, d: int,
-                 n_heads: int, cu_seqlens: Sequence[int], stream=None) -> torch.Tensor:
+                 n_heads: int, cu_seqlens: Sequence[int], stream=None,
+                 n_kv_heads: int = 0) -> torch.Tensor:
     cu = _cu_array(cu_seqlens)
     _check(lib().kraken_op_attention(dtype_code(qk.dtype), qk.data_ptr(), vt.data_ptr(),
-                                     out.data_ptr(), n, d, n_heads, cu, len(cu_seqlens) - 1,
-                                     _stream(stream)))
+                                     out.data_ptr(), n, d, n_heads, n_kv_heads, cu,
+                                     len(cu_seqlens) - 1, _stream(stream)))
     return out
 
 
 def op_decode_attention(qk: torch.Tensor, kv_layer: torch.Tensor, out: torch.Tensor, n: int,
                         d: int, n_heads: int, lens: Sequence[int], max_seqs: int, capacity: int,
-                        work: torch.Tensor, stream=None) -> None:
+                        work: torch.Tensor, stream=None, n_kv_heads: int = 0) -> None:
     """Attention of one new token per sequence over one layer of a KV cache."""
     B = len(lens)
     arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
@@ -381,5 +387,6 @@ def op_decode_attention(qk: torch.Tensor, kv_layer: torch.Tensor, out: torch.Ten
         raise ValueError("work must be float32")
     _check(lib().kraken_op_decode_attention(dtype_code(qk.dtype), qk.data_ptr(),
                                             kv_layer.data_ptr(), out.data_ptr(), n, d, n_heads,
-                                            arr, B, max_seqs, capacity, work.data_ptr(),
+                                            n_kv_heads, arr, B, max_seqs, capacity,
+                                            work.data_ptr(),
                                             work.numel(), _stream(stream)))

@@ -76,6 +76,9 @@ WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
              seq_lens=(8192,), compute="f16"),
     Workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16", 4, 36, 1280, 20, 5120, "bf16",
              ragged=(8, 512, 4096), compute="f16"),
+    # the benchmark shape with grouped-query attention: 4 key/value heads per sub-layer
+    Workload("kraken-n8-l24-d2048-h16-kv4-s8192-bf16", 8, 24, 2048, 16, 8192, "bf16",
+             seq_lens=(8192,), compute="f16", n_kv_heads=4),
 ]}
 
 # The workload the throughput benchmark runs: N=8 sub-layers of width 2048, 24 layers,

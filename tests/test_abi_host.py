@@ -117,3 +117,36 @@ def test_kv_cache_bytes():
         assert K().lib().kraken_kv_cache_bytes(ctypes.byref(c), ms, cap) == 0
     bad = K().Config(n_sub=0, n_layers=2, d_model=128, n_heads=4, max_tokens=4).c_struct()
     assert K().lib().kraken_kv_cache_bytes(ctypes.byref(bad), 1, 4) == 0
+
+
+def test_grouped_query_sizes():
+    # weight blob, KV cache and projection FLOPs with n_kv_heads key/value heads
+    N, L, d, F, H = 4, 3, 512, 1024, 16
+    hd = d // H
+    for Hkv in (16, 8, 4, 2):
+        dkv = Hkv * hd
+        cfg = K().Config(n_sub=N, n_layers=L, d_model=d, n_heads=H, d_ff=F, max_tokens=16,
+                         n_kv_heads=Hkv)
+        want = O.kraken_param_count(N, L, d, F, biases=True, layer_norms=True, w_concat=True,
+                                    kv_width=dkv)
+        assert K().weight_blob_elems(cfg) == want
+        c = cfg.c_struct()
+        assert K().lib().kraken_kv_cache_bytes(ctypes.byref(c), 2, 100) == \
+            L * N * 2 * 2 * 100 * dkv * 2
+        cu = [0, 100]
+        assert K().class_flops(cfg, K().K_GEMM_QK, cu) == L * N * 2.0 * 100 * d * (d + dkv)
+        assert K().class_flops(cfg, K().K_GEMM_VT, cu) == L * N * 2.0 * 100 * d * dkv
+    # n_kv_heads = n_heads is the multi-head model
+    a = K().Config(n_sub=N, n_layers=L, d_model=d, n_heads=H, d_ff=F, max_tokens=16)
+    b = K().Config(n_sub=N, n_layers=L, d_model=d, n_heads=H, d_ff=F, max_tokens=16,
+                   n_kv_heads=H)
+    assert K().weight_blob_elems(a) == K().weight_blob_elems(b)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_kv_heads=3), 1),                   # does not divide 4 heads
+    (dict(n_kv_heads=-1), 1),
+    (dict(d_model=256, n_heads=8, n_kv_heads=1), 2),   # 1 x 32 features: not a multiple of 64
+])
+def test_create_rejects_bad_kv_heads(kw, status):
+    assert _create_status(**kw) == status

@@ -77,7 +77,7 @@ def prefill_then_decode(w, lens, steps=2, seed=0, affine="random", capacity=None
 
     layers = [list(l) for l in oracle_layers(w, seed, affine)]
     out_o, _, kv = O.kraken_prefill(f64(X), cu, layers, wconcat(w, seed), w.n_heads,
-                                    return_kv=True)
+                                    return_kv=True, n_kv_heads=w.kv_heads)
     check("prefill out", out, out_o, tol(w))
     bound = tol(w)
     for j in range(w.n_layers):
@@ -98,7 +98,7 @@ def prefill_then_decode(w, lens, steps=2, seed=0, affine="random", capacity=None
         out_d, sub_d = model.decode(Xn, cur, cache, sub_out=True)
         torch.cuda.synchronize()
         out_do, sub_do, kv_new = O.kraken_decode(f64(Xn), cache_o, layers, wconcat(w, seed),
-                                                 w.n_heads)
+                                                 w.n_heads, n_kv_heads=w.kv_heads)
         check(f"step {step} out", out_d, out_do, bound)
         check(f"step {step} sub_out", sub_d, sub_do, bound)
         for j in range(w.n_layers):
@@ -163,7 +163,8 @@ def decode_over_standin_cache(w, lens, decode_tokens, seed=3, k_std=4.0):
     torch.cuda.synchronize()
     model.close()
     layers = [list(l) for l in oracle_layers(w, seed, "random")]
-    out_o, sub_o, _ = O.kraken_decode(f64(Xn), cache_o, layers, wconcat(w, seed), w.n_heads)
+    out_o, sub_o, _ = O.kraken_decode(f64(Xn), cache_o, layers, wconcat(w, seed), w.n_heads,
+                                      n_kv_heads=w.kv_heads)
     check("out", out, out_o, tol(w))
     check("sub_out", sub, sub_o, tol(w))
 
@@ -203,6 +204,25 @@ def test_decode_over_empty_cache_is_one_token_prefill(dtype):
     check("decode out", out, out_o, tol(w))
     check("decode sub_out", sub, sub_o, tol(w))
     check("prefill out", out_p, out_o, tol(w))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,Hkv,d", [(4, 2, 256), (4, 1, 256), (16, 2, 512), (16, 4, 512),
+                                     (6, 2, 384)])
+def test_grouped_query_prefill_kv_then_decode(dtype, H, Hkv, d):
+    # decode workgroups serve 4, 2 or 1 query heads of a key/value group (groups of 2, 4,
+    # 8 and 3 heads here); the cache holds Hkv heads
+    w = small(f"gqa-kv-n2-l2-d{d}-h{H}-kv{Hkv}", n_sub=2, d_model=d, n_heads=H, d_ff=2 * d,
+              dtype=dtype, n_kv_heads=Hkv)
+    prefill_then_decode(w, [3, 70, 33], steps=2)
+
+
+@pytest.mark.parametrize("H,Hkv", [(16, 4), (16, 1)])
+def test_grouped_query_decode_long_standin_cache(H, Hkv):
+    w = small(f"gqa-dec-n2-l1-d2048-h{H}-kv{Hkv}", n_sub=2, n_layers=1, d_model=2048,
+              n_heads=H, d_ff=2048, dtype="bf16", compute="f16", out_proj_std=0.05,
+              n_kv_heads=Hkv)
+    decode_over_standin_cache(w, [5000, 1], decode_tokens=2)
 
 
 def test_decode_and_prefill_kv_argument_errors():

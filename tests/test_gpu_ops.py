@@ -217,7 +217,40 @@ def test_attention(dtype, case):
                         f"attention sub-layer {i}")
 
 
-def check_attention(got, ref, qk64, vabs, cu, H, dtype, what):
+GQA_ATTN_CASES = [  # (n, d, heads, kv heads, seq_lens): groups of 2, 4, 8 and 3 heads
+    (2, 256, 4, 2, [300, 17]), (1, 256, 4, 1, [129, 200]), (2, 512, 16, 4, [130]),
+    (1, 2048, 16, 2, [257, 64]), (1, 384, 6, 2, [100]), (1, 512, 16, 2, [70]),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("case", GQA_ATTN_CASES)
+def test_attention_grouped_query(dtype, case):
+    n, d, H, Hkv, lens = case
+    dkv = Hkv * (d // H)
+    cu = [0]
+    for s in lens:
+        cu.append(cu[-1] + s)
+    T = cu[-1]
+    ldv = K().vt_ld(T)
+    dt = tdt(dtype)
+    g = torch.Generator(device="cpu").manual_seed(T * 7 + d + H + Hkv)
+    qk = (torch.randn((n, T, d + dkv), generator=g) * 1.5).to(dt).to(DEV)
+    v = torch.randn((n, T, dkv), generator=g).to(dt)
+    vt = torch.zeros((n, dkv, ldv), dtype=dt)
+    vt[:, :, :T] = v.transpose(1, 2)
+    vt = vt.to(DEV)
+    out = torch.full((n, T, d), float("nan"), dtype=dt, device=DEV)
+    K().op_attention(qk, vt, out, n, d, H, cu, n_kv_heads=Hkv)
+    torch.cuda.synchronize()
+    q64, v64 = f64(qk), f64(v)
+    for i in range(n):
+        ref = O.causal_attention(q64[i][:, :d], q64[i][:, d:], v64[i], cu, H, Hkv)
+        check_attention(f64(out[i]), ref, q64[i], np.abs(v64[i]), cu, H, dtype,
+                        f"grouped-query attention sub-layer {i}", d=d, Hkv=Hkv)
+
+
+def check_attention(got, ref, qk64, vabs, cu, H, dtype, what, d=None, Hkv=None):
     """Elementwise bound from the rounding model of the kernel.
 
     bf16: the probabilities p are rounded to bf16 (relative error <= 2^-8) before the
@@ -227,8 +260,8 @@ def check_attention(got, ref, qk64, vabs, cu, H, dtype, what):
     up to 128 terms, |s| up to ~30) moves each p by a relative ~1e-6 |s| through the
     exponential; 2^-16 covers it.
     """
-    d = qk64.shape[1] // 2
-    weighted_abs = O.causal_attention(qk64[:, :d], qk64[:, d:], vabs, cu, H)
+    d = d or qk64.shape[1] // 2
+    weighted_abs = O.causal_attention(qk64[:, :d], qk64[:, d:], vabs, cu, H, Hkv)
     u = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 2.0 ** -16}[dtype]
     bound = u * (weighted_abs + np.abs(ref)) + 1e-6 * np.sqrt(np.mean(ref ** 2))
     assert np.all(np.isfinite(got)), what
@@ -272,20 +305,43 @@ DECODE_ATTN_CASES = [
 @pytest.mark.parametrize("case", DECODE_ATTN_CASES)
 def test_decode_attention(dtype, case):
     n, d, H, lens, max_seqs, cap, splits = case
+    _check_decode_attention(dtype, n, d, H, H, lens, max_seqs, cap, splits)
+
+
+DECODE_GQA_CASES = [
+    # n, d, H, Hkv, lens, max_seqs, capacity, work splits: groups of 2, 4, 8 and 3 heads
+    # (workgroups of 2, 4, 4 and 1 query heads), chunk edges, an empty cache
+    (2, 256, 4, 2, [0, 255, 256, 1500], 4, 1600, None),
+    (1, 512, 16, 4, [3000, 1], 2, 3001, 3),
+    (1, 512, 16, 2, [777, 0], 2, 800, None),
+    (2, 384, 6, 2, [513, 40], 3, 600, None),
+    (1, 2048, 16, 1, [8192], 1, 8193, None),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("case", DECODE_GQA_CASES)
+def test_decode_attention_grouped_query(dtype, case):
+    n, d, H, Hkv, lens, max_seqs, cap, splits = case
+    _check_decode_attention(dtype, n, d, H, Hkv, lens, max_seqs, cap, splits)
+
+
+def _check_decode_attention(dtype, n, d, H, Hkv, lens, max_seqs, cap, splits):
     hd, B = d // H, len(lens)
+    dkv = Hkv * hd
     dt = tdt(dtype)
-    g = torch.Generator(device="cpu").manual_seed(sum(lens) + 7 * d + n)
-    qk = (torch.randn((n, B, 2 * d), generator=g) * 2.0).to(dt)
-    cache = torch.full((n, 2, max_seqs, H, cap, hd), float("nan"), dtype=dt)
+    g = torch.Generator(device="cpu").manual_seed(sum(lens) + 7 * d + n + 31 * Hkv)
+    qk = (torch.randn((n, B, d + dkv), generator=g) * 2.0).to(dt)
+    cache = torch.full((n, 2, max_seqs, Hkv, cap, hd), float("nan"), dtype=dt)
     rows_k, rows_v = [], []
     for i in range(n):
         rk, rv = [], []
         for b in range(B):
             # keys and values at positions 0..lens[b]; the new token's own at lens[b]
-            k = (torch.randn((lens[b] + 1, d), generator=g) * 2.0).to(dt)
-            v = torch.randn((lens[b] + 1, d), generator=g).to(dt)
-            cache[i, 0, b, :, :lens[b] + 1] = k.view(-1, H, hd).transpose(0, 1)
-            cache[i, 1, b, :, :lens[b] + 1] = v.view(-1, H, hd).transpose(0, 1)
+            k = (torch.randn((lens[b] + 1, dkv), generator=g) * 2.0).to(dt)
+            v = torch.randn((lens[b] + 1, dkv), generator=g).to(dt)
+            cache[i, 0, b, :, :lens[b] + 1] = k.view(-1, Hkv, hd).transpose(0, 1)
+            cache[i, 1, b, :, :lens[b] + 1] = v.view(-1, Hkv, hd).transpose(0, 1)
             rk.append(f64(k))
             rv.append(f64(v))
         rows_k.append(rk)
@@ -293,7 +349,8 @@ def test_decode_attention(dtype, case):
     per_split = n * B * H * (hd + 2)
     work = torch.empty(per_split * (splits or 64), dtype=torch.float32, device=DEV)
     out = torch.full((n, B, d), float("nan"), dtype=dt, device=DEV)
-    K().op_decode_attention(qk.to(DEV), cache.to(DEV), out, n, d, H, lens, max_seqs, cap, work)
+    K().op_decode_attention(qk.to(DEV), cache.to(DEV), out, n, d, H, lens, max_seqs, cap, work,
+                            n_kv_heads=Hkv)
     torch.cuda.synchronize()
     q64 = f64(qk)
     for i in range(n):
@@ -302,8 +359,9 @@ def test_decode_attention(dtype, case):
         v_new = np.stack([rows_v[i][b][-1] for b in range(B)])
         K_c = [rows_k[i][b][:-1] for b in range(B)]
         V_c = [rows_v[i][b][:-1] for b in range(B)]
-        ref = O.cached_attention(q, k_new, v_new, K_c, V_c, H)
-        wabs = O.cached_attention(q, k_new, np.abs(v_new), K_c, [np.abs(x) for x in V_c], H)
+        ref = O.cached_attention(q, k_new, v_new, K_c, V_c, H, Hkv)
+        wabs = O.cached_attention(q, k_new, np.abs(v_new), K_c, [np.abs(x) for x in V_c], H,
+                                  Hkv)
         # fp32 scores, probabilities and accumulation; one rounding of the output to S
         u = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 0.0}[dtype]
         bound = u * np.abs(ref) + 2.0 ** -16 * wabs + 1e-6 * np.sqrt(np.mean(ref ** 2))

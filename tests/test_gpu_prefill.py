@@ -43,7 +43,7 @@ def say(msg):
 def cfg_of(w, T):
     return K().Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
                       n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=T, dtype=w.dtype,
-                      compute=w.compute)
+                      compute=w.compute, n_kv_heads=w.n_kv_heads)
 
 
 def build_model(w, T, seed=0, affine="plain"):
@@ -89,7 +89,8 @@ def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
         cu_o = synth.cu_seqlens([min(prefix, s) for s in lens])
     Xo = f64(X)[rows]
     out_o, sub_o = O.kraken_prefill(Xo, cu_o, oracle_layers(w, seed, affine),
-                                    f64(synth.gen_w_concat(w, seed, DEV)), w.n_heads)
+                                    f64(synth.gen_w_concat(w, seed, DEV)), w.n_heads,
+                                    n_kv_heads=w.kv_heads)
     e_out = rel_err(f64(out)[rows], out_o)
     e_sub = rel_err(f64(sub)[:, rows], sub_o)
     say(f"    max|err|/rms: out {e_out:.3e}  sub_out {e_sub:.3e}  (bound {TOL[w.dtype]})")
@@ -132,6 +133,18 @@ def test_single_sub_layer_single_token():
     w = small("n1-l2-d128-h2", n_sub=1, n_layers=2, d_model=128, n_heads=2, d_ff=256, dtype="f32")
     run_and_compare(w, [1], affine="random")
     run_and_compare(w, [1, 1, 1], affine="random")
+
+
+# ----------------------------------------- grouped-query and multi-query attention, in full
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,Hkv,d", [(4, 2, 256), (4, 1, 256), (2, 1, 256), (8, 2, 256),
+                                     (16, 4, 512)])
+def test_grouped_query_attention(dtype, H, Hkv, d):
+    # query head h reads key/value head h // (H / Hkv); head sizes 64, 128 and 32
+    w = small(f"gqa-n2-l2-d{d}-h{H}-kv{Hkv}", n_sub=2, d_model=d, n_heads=H, d_ff=2 * d,
+              dtype=dtype, n_kv_heads=Hkv)
+    run_and_compare(w, [130, 7, 300], affine="random")
 
 
 # ------------------------------------------------------- benchmark-size workloads, prefix
