@@ -39,8 +39,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "1a0cd80a98d02e09c33064c9a7128ce40a1ef4d094f44f092fea90a51a400da3",
-        "read_bytes": 3155395201, "write_bytes": 269239748,
+        "source_sha256": "adc32da9560f3b1f18733c4334b274215280b5b061154515e0ca0f55a890acd6",
+        "read_bytes": 3266975313, "write_bytes": 268949712,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
@@ -48,8 +48,8 @@ TRAFFIC = {
     # kernel plus its chunk merge
     "decode_attention_b1_ctx8192": {
         "source": "paper_2408_07802_amd/csrc/decode.hip",
-        "source_sha256": "f257057f7424fbdb26c7ae48337e7b4c66b7e6bf64456eb67cd49804c6fccbb0",
-        "read_bytes": 538083507, "write_bytes": 659456,
+        "source_sha256": "99e0f0ad725281d6d4539686de8880789824f406a41a1b9aa754bd2759fc5ad8",
+        "read_bytes": 537730065, "write_bytes": 450560,
         "algorithmic_bytes": 537034752,
         "profile": "profiles/hbm_traffic_decode_n8_l24_d2048_ctx8192.md",
     },

@@ -162,12 +162,48 @@ __device__ __forceinline__ float xor_max_from(float v) {
   for (int o = FROM; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
 }
-// Sum over the lanes of one aligned group of UPTO lanes.
+// Lane x of a DPP pattern (a VALU operand modifier: no LDS traffic).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
+                                                               CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the lanes of one aligned group of UPTO lanes, in every lane of the group.  Up to
+// 16 lanes with DPP adds: the quad permutations [1,0,3,2] and [2,3,0,1] pair lanes 1 and 2
+// apart, the half-row mirror pairs each lane of a 4-lane quad with one of the other quad,
+// and the row mirror each lane of an 8-lane half with one of the other half.
 template <int UPTO>
-__device__ __forceinline__ float xor_sum_below(float v) {
-#pragma unroll
-  for (int o = 1; o < UPTO; o <<= 1) v += __shfl_xor(v, o, 64);
+__device__ __forceinline__ float group_sum(float v) {
+  if constexpr (UPTO >= 2) v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+  if constexpr (UPTO >= 4) v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+  if constexpr (UPTO >= 8) v += dpp_f<0x141>(v);   // row_half_mirror
+  if constexpr (UPTO >= 16) v += dpp_f<0x140>(v);  // row_mirror
+  if constexpr (UPTO >= 32) v += __shfl_xor(v, 16, 64);
+  if constexpr (UPTO >= 64) v += __shfl_xor(v, 32, 64);
   return v;
+}
+
+// Dot product of a 16-byte chunk of a key row with the matching query elements, fp32
+// accumulation: v_dot2 on 16-bit pairs (exact products, fp32 sums), fp32 FMAs otherwise.
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+template <typename S>
+__device__ __forceinline__ float chunk_dot(uint4 k, uint4 q) {
+  if constexpr (__is_same(S, f16)) {
+    float a = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, k.x), __builtin_bit_cast(f16x2, q.x), 0.f, false);
+    a = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, k.y), __builtin_bit_cast(f16x2, q.y), a, false);
+    a = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, k.z), __builtin_bit_cast(f16x2, q.z), a, false);
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, k.w), __builtin_bit_cast(f16x2, q.w), a, false);
+  } else if constexpr (__is_same(S, bf16)) {
+    float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.x), __builtin_bit_cast(bf16x2, q.x), 0.f, false);
+    a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.y), __builtin_bit_cast(bf16x2, q.y), a, false);
+    a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.z), __builtin_bit_cast(bf16x2, q.z), a, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k.w), __builtin_bit_cast(bf16x2, q.w), a, false);
+  } else {
+    const float4 kf = __builtin_bit_cast(float4, k), qf = __builtin_bit_cast(float4, q);
+    return fmaf(kf.w, qf.w, fmaf(kf.z, qf.z, fmaf(kf.y, qf.y, kf.x * qf.x)));
+  }
 }
 
 // Workgroup (sub-layer i, sequence b, query heads h0 .. h0+QG-1, chunk s) over keys
@@ -205,16 +241,13 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecAttnParams p) {
   const int nkeys = p.lens[b] + 1;
   const int k_begin = s * p.chunk, k_end = min(k_begin + p.chunk, nkeys);
 
-  float q[QG][EPC];
+  // this lane's chunk of each query, as stored (the scale applies to the fp32 score)
+  uint4 q[QG];
 #pragma unroll
-  for (int g = 0; g < QG; ++g) {
-    const S* qp = static_cast<const S*>(p.qk) + ((int64_t)i * p.B + b) * (p.d + p.dkv) +
-                  (h0 + g) * HD + c * EPC;
-    const uint4 ch = *reinterpret_cast<const uint4*>(qp);
-    const S* e = reinterpret_cast<const S*>(&ch);
-#pragma unroll
-    for (int u = 0; u < EPC; ++u) q[g][u] = to_f(e[u]) * p.scale;
-  }
+  for (int g = 0; g < QG; ++g)
+    q[g] = *reinterpret_cast<const uint4*>(static_cast<const S*>(p.qk) +
+                                           ((int64_t)i * p.B + b) * (p.d + p.dkv) +
+                                           (h0 + g) * HD + c * EPC);
   const S* cache = static_cast<const S*>(p.cache);
   const S* Kb = cache + cache_index(i, 0, b, hkv, 0, 0, p.max_seqs, p.Hkv, p.cap, HD) + c * EPC;
   const S* Vb = cache + cache_index(i, 1, b, hkv, 0, 0, p.max_seqs, p.Hkv, p.cap, HD) + c * EPC;
@@ -247,11 +280,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecAttnParams p) {
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < R; ++j) {
-        const S* e = reinterpret_cast<const S*>(&kr[j]);
-        float a = 0.f;
-#pragma unroll
-        for (int u = 0; u < EPC; ++u) a = fmaf(to_f(e[u]), q[g][u], a);
-        a = xor_sum_below<LPR>(a);             // the row's full dot product, in every lane
+        // the row's full dot product, in every lane of its group
+        const float a = group_sum<LPR>(chunk_dot<S>(kr[j], q[g])) * p.scale;
         sc[j] = kb + j * RPP + row0 < k_end ? a : -INFINITY;
         mx = fmaxf(mx, sc[j]);
       }
@@ -427,17 +457,19 @@ hipError_t launch_decode_attention(DType dt, const void* qk, const void* cache_l
   const int group = n_heads / kvh, qg = heads_per_workgroup(group);
   int max_keys = 1;
   for (int b = 0; b < B; ++b) max_keys = max(max_keys, lens_host[b] + 1);
-  // Chunks of 256 .. 1024 keys (whole 256-key units) sized for about 1024 workgroups:
-  // longer chunks amortise each workgroup's query load and final merge (measured on
-  // 8192 cached keys: 1024-key chunks 15% faster than 256-key ones for one sequence,
-  // 4% for eight); the chunk grows further when the partial buffer is too small.
+  // Chunks of 256 .. 1536 keys (whole 256-key units) sized for about 384 workgroups: long
+  // chunks amortise each workgroup's query loads and final merge.  Measured at N=8, 16
+  // query heads of 128, 8192 cached keys: 16 key/value heads, one sequence 1536-key chunks
+  // 96 us against 119 us with 256; 4 key/value heads, one sequence 768-key chunks 38 us
+  // against 48 us; eight sequences 1536 keys best in both.  The chunk grows further when
+  // the partial buffer is too small.
   const int64_t per_split = decode_partial_floats(n, B, n_heads, hd, 1);
   const int64_t max_splits = part_floats / per_split;
   if (max_splits < 1) return hipErrorInvalidValue;
   const int64_t per_chunk_wgs = (int64_t)n * B * (n_heads / qg);
   const int64_t want =
-      ((int64_t)max_keys * per_chunk_wgs / 1024 + DEC_KEYS - 1) / DEC_KEYS * DEC_KEYS;
-  int chunk = (int)std::min<int64_t>(std::max<int64_t>(want, DEC_KEYS), 4 * DEC_KEYS);
+      ((int64_t)max_keys * per_chunk_wgs / 384 + DEC_KEYS - 1) / DEC_KEYS * DEC_KEYS;
+  int chunk = (int)std::min<int64_t>(std::max<int64_t>(want, DEC_KEYS), 6 * DEC_KEYS);
   while ((max_keys + chunk - 1) / chunk > max_splits) chunk += DEC_KEYS;
   DecAttnParams p;
   p.qk = qk; p.cache = cache_layer; p.part = part;
