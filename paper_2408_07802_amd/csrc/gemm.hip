@@ -471,11 +471,10 @@ __device__ __forceinline__ f32x4 mfma16(uint4 a, uint4 b, f32x4 c) {
 
 constexpr int SK_UNROLL = 8;   // steps of 32 k whose loads are issued together
 
-// 16-byte streaming load: weights are read once per step, so they need not stay cached.
-typedef unsigned int u32v4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 load_stream16(const void* ptr) {
-  const u32v4 v = __builtin_nontemporal_load(reinterpret_cast<const u32v4*>(ptr));
-  return make_uint4(v[0], v[1], v[2], v[3]);
+// 16-byte weight load (plain: non-temporal loads measured the same, within 3%, on weight
+// streams that do not fit the last-level cache).
+__device__ __forceinline__ uint4 load_w16(const void* ptr) {
+  return *reinterpret_cast<const uint4*>(ptr);
 }
 
 template <typename S, int MB, int TW, int EPI>
@@ -536,7 +535,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmParams p) {
 #pragma unroll
     for (int u = 0; u < SK_UNROLL; ++u)
 #pragma unroll
-      for (int w = 0; w < TW; ++w) bv[u][w] = load_stream16(Bz[w] + bo[u]);
+      for (int w = 0; w < TW; ++w) bv[u][w] = load_w16(Bz[w] + bo[u]);
 #pragma unroll
     for (int u = 0; u < SK_UNROLL; ++u)
 #pragma unroll
@@ -553,7 +552,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmParams p) {
   for (; t < t1; ++t) {
     uint4 bv[TW];
 #pragma unroll
-    for (int w = 0; w < TW; ++w) bv[w] = load_stream16(Bz[w] + gb * p.gB + kk);
+    for (int w = 0; w < TW; ++w) bv[w] = load_w16(Bz[w] + gb * p.gB + kk);
     const int64_t ao = g * p.gA + kk;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -617,16 +616,16 @@ hipError_t launch_skinny(const GemmDesc& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Two 16-column blocks per wave (each A fragment feeds two MFMAs, halving A loads per
-// weight byte) unless that leaves one row with fewer than 1024 workgroups, where the
-// longer per-wave reductions cost more than the A loads save (measured on the N=8,
-// d=2048 decode projections: FFN down at one row 9% slower with two blocks, every
-// projection at eight rows 10-25% faster).
+// Two 16-column blocks per wave (each A fragment feeds two MFMAs, halving the A loads per
+// weight byte) for several rows and reductions up to 4096; one block (twice the
+// workgroups) otherwise.  Measured on the N=8, d=2048 decode projections with weights
+// streamed from HBM: one row, one block 5-18% faster for every projection (FFN down 54
+// against 66 us); eight rows, two blocks 4-5% faster at K = 2048, one block 5% faster at
+// K = 8192.
 template <typename S, int MB>
 hipError_t launch_skinny_tw(const GemmDesc& g, hipStream_t s) {
-  const int64_t wgs2 = (int64_t)((g.N + 31) / 32) * g.batch;
-  if (g.M == 1 && wgs2 < 1024) return launch_skinny<S, MB, 1>(g, s);
-  return launch_skinny<S, MB, 2>(g, s);
+  if (g.M > 1 && (int64_t)g.K * g.kgroups <= 4096) return launch_skinny<S, MB, 2>(g, s);
+  return launch_skinny<S, MB, 1>(g, s);
 }
 
 template <typename S>

@@ -103,7 +103,7 @@ GEMM_BIG_SHAPES = [(2000, 1100, 320, 15), (1024, 1024, 64, 32)]
 # 8 steps of 32 k plus a remainder, 1, 2 or 4 blocks of 16 rows
 GEMM_SKINNY_SHAPES = [(1, 2048, 8192, 2), (5, 1000, 2048, 3), (16, 4096, 2048, 1),
                       (17, 33, 320, 2), (33, 130, 64, 1), (64, 2048, 1024, 2),
-                      (9, 520, 2112, 2), (3, 7, 64, 1), (1, 4096, 2048, 8)]
+                      (9, 520, 2112, 2), (3, 7, 64, 1), (1, 4096, 2048, 8), (20, 300, 8192, 2)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
