@@ -15,6 +15,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                                         (one decode step of B sequences of C cached
                                           tokens each: decode tokens/s and an HBM
                                           roofline of its dominant kernel)
+       python bench.py --share G        (one GPU's part of a G-way split: N/G
+                                          sub-layers per layer, no exchange)
 """
 
 import argparse
@@ -265,6 +267,8 @@ def main():
     ap.add_argument("--phase", choices=["prefill", "decode"], default="prefill")
     ap.add_argument("--batch", type=int, default=1, help="decode: sequences per step")
     ap.add_argument("--context", type=int, default=8192, help="decode: cached tokens each")
+    ap.add_argument("--share", type=int, default=1,
+                    help="run one GPU's share of a G-way split: N/G sub-layers per layer")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -281,6 +285,15 @@ def main():
     w = synth.workload(args.workload or synth.BENCH_WORKLOAD)
     if args.compute:
         w = dataclasses.replace(w, compute=args.compute)
+    if args.share > 1:
+        # one GPU's part of a G-way Kraken (Section 3.1: the N sub-layers split over G
+        # devices): N/G sub-layers at the full depth, width and length.  The exchange of the
+        # per-layer partial sums is not run, so each layer's combine sums the local
+        # sub-layers only; the arithmetic per GPU is the sharded model's.
+        if w.n_sub % args.share:
+            raise SystemExit(f"--share {args.share} does not divide N = {w.n_sub}")
+        w = dataclasses.replace(w, name=f"{w.name}-share1of{args.share}",
+                                n_sub=w.n_sub // args.share)
     compute = w.dtype if w.compute == "storage" else w.compute
     if args.phase == "decode":
         bench_decode(args, w, compute)
