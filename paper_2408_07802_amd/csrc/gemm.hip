@@ -238,11 +238,13 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // Fragment reads (uint4 index inside the ring).  Row r of a tile holds its logical
-  // chunk k at physical chunk k ^ swz_key(r); for fragment row wm*TM + 32i + lrow that key
-  // is swz_key(lrow) ^ 4(i & 1) because TM and TN are multiples of 64.
-  static_assert(TM % 64 == 0 || TM == 32, "fragment swizzle identity needs TM % 64 == 0");
+  // chunk k at physical chunk k ^ swz_key(r); for fragment row base + 32i + lrow (base =
+  // wm*TM for A, BM + wn*TN for B, multiples of 32, BM of 64) that key is
+  // swz_key(lrow) ^ 4((base/32 + i) & 1).
+  static_assert(TM % 32 == 0 && TN % 32 == 0 && BM % 64 == 0, "fragment row bases");
   const int arow = (wm * TM + lrow) * CH, brow = (BM + wn * TN + lrow) * CH;
   const int sw = swz_key(lrow);
+  const int apar = (wm * (TM / 32)) & 1, bpar = (wn * (TN / 32)) & 1;
   uint4 af[2][FM], bfr[2][FN];
   // Read k of a chunk: 0 -> A block 0, 1..FN -> B blocks, then A blocks 1..FM-1, the order
   // in which the chunk's MFMAs (i outer, j inner) first need them.
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
     constexpr int k = decltype(K)::value;
     constexpr bool is_a = k == 0 || k > FN;
     constexpr int idx = k == 0 ? 0 : (k <= FN ? k - 1 : k - FN);
-    const int ch = ((2 * c + lhalf) ^ sw) ^ ((idx & 1) * 4);
+    const int ch = ((2 * c + lhalf) ^ sw) ^ (((idx + (is_a ? apar : bpar)) & 1) * 4);
     if constexpr (is_a)
       af[slot][idx] = lds[stage_idx + arow + idx * 32 * CH + ch];
     else
@@ -650,17 +652,24 @@ hipError_t launch_gemm(const GemmDesc& g, hipStream_t s) {
     if (g.dt == DType::BF16) return launch_skinny_rows<bf16>(g, s);
     return launch_skinny_rows<f16>(g, s);
   }
-  // 256 x 256 tiles when they give at least two waves of workgroups over the 256 CUs,
-  // else 128 x 128 (small token counts or narrow projections).
+  // 256 x 256 tiles when they give at least two waves of workgroups over the 256 CUs, else
+  // 128 x 128, and 128 x 64 when those leave CUs idle (a prompt of ~100-200 tokens, where
+  // the projections stream their weights and need workgroups in flight; measured on the
+  // 65B and 175B 4-way engine shapes at 128 tokens: 156-232 workgroups of 128 x 128 ->
+  // 128 x 64 7-10% faster, 464 -> 128 x 64 40% slower).
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.batch;
-  const bool use_big = big >= 512;
+  const int64_t mid = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128) * g.batch;
+  const int cfg = big >= 512 ? 2 : mid >= 256 ? 1 : 0;
   switch (g.dt) {
     case DType::BF16:
-      return use_big ? launch_cfg<bf16, 256, 256>(g, s) : launch_cfg<bf16, 128, 128>(g, s);
+      return cfg == 2 ? launch_cfg<bf16, 256, 256>(g, s)
+           : cfg == 1 ? launch_cfg<bf16, 128, 128>(g, s) : launch_cfg<bf16, 128, 64>(g, s);
     case DType::F16:
-      return use_big ? launch_cfg<f16, 256, 256>(g, s) : launch_cfg<f16, 128, 128>(g, s);
+      return cfg == 2 ? launch_cfg<f16, 256, 256>(g, s)
+           : cfg == 1 ? launch_cfg<f16, 128, 128>(g, s) : launch_cfg<f16, 128, 64>(g, s);
     default:
-      return use_big ? launch_cfg<float, 256, 256>(g, s) : launch_cfg<float, 128, 128>(g, s);
+      return cfg == 2 ? launch_cfg<float, 256, 256>(g, s)
+           : cfg == 1 ? launch_cfg<float, 128, 128>(g, s) : launch_cfg<float, 128, 64>(g, s);
   }
 }
 

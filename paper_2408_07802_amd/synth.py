@@ -79,6 +79,17 @@ WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
     # the benchmark shape with grouped-query attention: 4 key/value heads per sub-layer
     Workload("kraken-n8-l24-d2048-h16-kv4-s8192-bf16", 8, 24, 2048, 16, 8192, "bf16",
              seq_lens=(8192,), compute="f16", n_kv_heads=4),
+    # the paper's 4-way Kraken engines of the 65B and 175B models (engine table: d_ff = 2d,
+    # heads per sub-layer), built like the paper's with a quarter of the layers, fp16, one
+    # sequence of 128 or 2048 tokens
+    Workload("kraken-n4-l20-d4992-h39-f9984-s2048-f16", 4, 20, 4992, 39, 9984, "f16",
+             seq_lens=(2048,)),
+    Workload("kraken-n4-l20-d4992-h39-f9984-s128-f16", 4, 20, 4992, 39, 9984, "f16",
+             seq_lens=(128,)),
+    Workload("kraken-n4-l24-d7424-h58-f14848-s2048-f16", 4, 24, 7424, 58, 14848, "f16",
+             seq_lens=(2048,)),
+    Workload("kraken-n4-l24-d7424-h58-f14848-s128-f16", 4, 24, 7424, 58, 14848, "f16",
+             seq_lens=(128,)),
 ]}
 
 # The workload the throughput benchmark runs: N=8 sub-layers of width 2048, 24 layers,

@@ -23,7 +23,7 @@ from paper_2408_07802_amd import synth
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
-TOL = {"bf16": 2e-2, "f32": 1e-4}
+TOL = {"bf16": 2e-2, "f16": 2e-2, "f32": 1e-4}
 
 
 def K():
@@ -133,6 +133,22 @@ def test_single_sub_layer_single_token():
     w = small("n1-l2-d128-h2", n_sub=1, n_layers=2, d_model=128, n_heads=2, d_ff=256, dtype="f32")
     run_and_compare(w, [1], affine="random")
     run_and_compare(w, [1, 1, 1], affine="random")
+
+
+# --------------------------------------------------------- head counts of the engine table
+
+def test_odd_head_count():
+    # 5 heads of 64 (the engine table has 39-, 57- and 58-head sub-layers)
+    w = small("odd-n2-l2-d320-h5", n_sub=2, d_model=320, n_heads=5, d_ff=640, dtype="f16")
+    run_and_compare(w, [200, 71], affine="random")
+
+
+def test_head_group_order_with_a_remainder_group():
+    # 4 sub-layers x 58 heads = 232 (sub-layer, head) pairs, 29 per XCD: groups of 4 with a
+    # last group of 1, in the grouped workgroup order (232 x 9 query tiles >= 2048)
+    w = small("h58-n4-l1-d1856-h58", n_sub=4, n_layers=1, d_model=1856, n_heads=58,
+              d_ff=1856, dtype="f16")
+    run_and_compare(w, [2304], affine="plain")
 
 
 # ----------------------------------------- grouped-query and multi-query attention, in full
