@@ -185,6 +185,23 @@ def test_n8_l24_d2048_s8192_prefix():
     run_and_compare(w, synth.seq_lens(w), prefix=96)
 
 
+def test_n8_l24_d2048_s8192_first_half_equals_4096_token_prefill():
+    # causal prefix invariance at the benchmark's launch configuration: rows 0..4095 of the
+    # 8192-token prefill against a 4096-token prefill of the same tokens (a property of
+    # the method that holds at any size; the oracle checks the first rows of each)
+    w = synth.workload("kraken-n8-l24-d2048-h16-s8192-bf16")
+    model = build_model(w, 8192)
+    X = synth.gen_hidden(w, 8192, 0, DEV)
+    out_f, sub_f = model.prefill(X, [0, 8192], sub_out=True)
+    out_h, sub_h = model.prefill(X[:4096].contiguous(), [0, 4096], sub_out=True)
+    torch.cuda.synchronize()
+    model.close()
+    e_out = rel_err(f64(out_f[:4096]), f64(out_h))
+    e_sub = rel_err(f64(sub_f[:, :4096]), f64(sub_h))
+    say(f"    rows 0..4095 of 8192 vs 4096 tokens: out {e_out:.3e} sub_out {e_sub:.3e}")
+    assert e_out <= 1e-6 and e_sub <= 1e-6
+
+
 def test_n4_l36_d1280_ragged8_prefix():
     w = synth.workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16")
     run_and_compare(w, synth.seq_lens(w), prefix=40)
