@@ -41,9 +41,17 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "adc32da9560f3b1f18733c4334b274215280b5b061154515e0ca0f55a890acd6",
-        "read_bytes": 3266975313, "write_bytes": 268949712,
+        "source_sha256": "1b2e345a7c120ac2b18cc0e75ad6bb506a9579a5ed8b73d8740864c074bb406a",
+        "read_bytes": 3230405818, "write_bytes": 269484630,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
+        "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
+    },
+    # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
+    "gemm_up": {
+        "source": "paper_2408_07802_amd/csrc/gemm.hip",
+        "source_sha256": "9f601deb3bbeb5efc108ead2d229be36f65c514f102377f2ce96cccc68bca255",
+        "read_bytes": 3233684931, "write_bytes": 1073767792,
+        "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
     # decode step, one sequence of 8192 cached tokens: the attention class is the split-key
