@@ -10,16 +10,17 @@
 // width d), so one launch covers a whole layer's projection.
 //
 // Tiling (gfx950): a workgroup of 4 waves (2 x 2) computes a BM x BN tile
-// (256 x 256 or 128 x 128); each wave owns a (BM/2) x (BN/2) sub-tile of 32x32
+// (256 x 256, 128 x 128 or 128 x 64); each wave owns a (BM/2) x (BN/2) sub-tile of 32x32
 // MFMA blocks (v_mfma_f32_32x32x16_{bf16,f16} for 16-bit operands,
 // v_mfma_f32_32x32x2_f32 for fp32).  K advances in 128-byte slices (64 16-bit or
 // 32 fp32 elements).  Operand tiles go from HBM straight into LDS with
-// global_load_lds_dwordx4 (no register staging) into the other half of a
-// double-buffered LDS ring while the MFMAs consume the current half.  Tile rows
-// are 128 bytes; 16-byte chunk c of row r is stored at chunk c ^ swz_key(r), which
-// keeps fragment reads free of bank conflicts.  The swizzle is applied on the load
-// side: each lane of a DMA load writes the next 16 bytes of LDS, so it fetches the
-// logical chunk that belongs there.  The main loop's instruction order is fixed by
+// global_load_lds_dwordx4 (no register staging) into a ring of five operand-tile slots
+// (the whole 160 KB LDS at 256 x 256): while the MFMAs consume slice s, the B tile of
+// slice s+1 and the A tile of slice s+2 are loading, so A tiles get two slices of
+// MFMAs to arrive and B tiles one.  Tile rows are 128 bytes; 16-byte chunk c of row r
+// is stored at chunk c ^ swz_key(r), which keeps fragment reads free of bank conflicts.
+// The swizzle is applied on the load side: each lane of a DMA load writes the next 16
+// bytes of LDS, so it fetches the logical chunk that belongs there.  The main loop's instruction order is fixed by
 // hand (fragment reads and DMAs interleaved one per MFMA, one barrier per slice) so
 // that the single wave per SIMD keeps the matrix pipe busy.
 // Rows past M (or N) load a clamped in-bounds row; they only feed outputs that
@@ -141,16 +142,16 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   constexpr int TM = BM / 2, TN = BN / 2;      // wave tile
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int AI = BM / 32, BI = BN / 32;    // DMA instructions per wave per slice
-  constexpr int STAGE = (BM + BN) * CH;        // uint4 per LDS stage
+  constexpr int SLOT = (BM > BN ? BM : BN) * CH;  // uint4 per ring slot (one operand tile)
+  constexpr int NSLOT = 5;                     // ring slots: 2.5 slices of A and B tiles
   constexpr int NCH = CH / 2;                  // 16-byte-per-lane K chunks per slice
   constexpr int NM = FM * FN;                  // MFMA blocks per chunk
   constexpr int NR = FM + FN;                  // fragment reads per chunk
-  constexpr int ND = AI + BI;                  // DMA instructions per wave per slice
   constexpr int BAR = NM * 3 / 4;              // last-chunk MFMA slot of the barrier
-  constexpr int DCH = 2;                       // chunks the slice's DMAs spread over
-  static_assert(DCH < NCH && BAR < NM, "schedule slots out of range");
+  static_assert(NCH == 4 && BAR < NM, "schedule slots out of range");
+  static_assert(AI == 4 || AI == 8, "vmcnt immediates below cover 4 or 8 A DMAs");
 
-  __shared__ uint4 lds[2 * STAGE];
+  __shared__ uint4 lds[NSLOT * SLOT];
 
   // ---- tile scheduling: XCD-aware remap, then grouped raster inside a batch entry
   const int tiles_per_batch = p.tiles_m * p.tiles_n;
@@ -199,34 +200,42 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   const uint32_t lds_base =
       __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)lds);
   const uint32_t a_dst = lds_base + (uint32_t)(wave * (BM / 4)) * 128u;
-  const uint32_t b_dst = lds_base + (uint32_t)(BM + wave * (BN / 4)) * 128u;
+  const uint32_t b_dst = lds_base + (uint32_t)(wave * (BN / 4)) * 128u;
 
-  // Source of the next slice to load: (K group, k offset) advanced one slice at a time.
+  // Sources of the next A and B slices to load, each a (K group, k offset) pair advanced
+  // one slice at a time: A runs two slices ahead of the MFMAs, B one.
   const int ksl = p.K / BK;                // slices per K group
   const int nsl = ksl * p.kgroups;         // total slices
   const char* a_src = reinterpret_cast<const char*>(Az);
   const char* b_src = reinterpret_cast<const char*>(Bz);
-  int ld_k = 0, ld_g = 0, ld_bg = 0;
-  auto advance_src = [&]() {
-    if (++ld_k < ksl) {
+  int a_k = 0, a_g = 0, b_k = 0, b_bg = 0;
+  auto advance_a = [&]() {
+    if (++a_k < ksl) {
       a_src += BK * sizeof(S);
-      b_src += BK * sizeof(S);
     } else {
-      ld_k = 0;
-      ++ld_g;
-      if (++ld_bg == p.gBmod) ld_bg = 0;
-      a_src = reinterpret_cast<const char*>(Az + ld_g * p.gA);
-      b_src = reinterpret_cast<const char*>(Bz + ld_bg * p.gB);
+      a_k = 0;
+      ++a_g;
+      a_src = reinterpret_cast<const char*>(Az + a_g * p.gA);
     }
   };
-  // DMA instruction u (A rows first, then B rows) of the current source slice into the
-  // stage at byte offset `stage`.
-  auto dma_item = [&](uint32_t stage, auto U) {
+  auto advance_b = [&]() {
+    if (++b_k < ksl) {
+      b_src += BK * sizeof(S);
+    } else {
+      b_k = 0;
+      if (++b_bg == p.gBmod) b_bg = 0;
+      b_src = reinterpret_cast<const char*>(Bz + b_bg * p.gB);
+    }
+  };
+  // DMA instruction u of the current A (or B) source slice into the ring slot at byte
+  // offset `slot`.
+  auto dma_a = [&](uint32_t slot, auto U) {
     constexpr int u = decltype(U)::value;
-    if constexpr (u < AI)
-      dma16(a_dst + stage + u * 1024u, a_src, aoff[u]);
-    else
-      dma16(b_dst + stage + (u - AI) * 1024u, b_src, boff[u - AI]);
+    dma16(a_dst + slot + u * 1024u, a_src, aoff[u]);
+  };
+  auto dma_b = [&](uint32_t slot, auto U) {
+    constexpr int u = decltype(U)::value;
+    dma16(b_dst + slot + u * 1024u, b_src, boff[u]);
   };
 
   f32x16 acc[FM][FN];
@@ -237,49 +246,73 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Fragment reads (uint4 index inside the ring).  Row r of a tile holds its logical
-  // chunk k at physical chunk k ^ swz_key(r); for fragment row base + 32i + lrow (base =
-  // wm*TM for A, BM + wn*TN for B, multiples of 32, BM of 64) that key is
+  // Fragment reads (uint4 index inside the ring).  Row r of an operand tile holds its
+  // logical chunk k at physical chunk k ^ swz_key(r); for fragment row base + 32i + lrow
+  // (base = wm*TM for A, wn*TN for B, multiples of 32) that key is
   // swz_key(lrow) ^ 4((base/32 + i) & 1).
-  static_assert(TM % 32 == 0 && TN % 32 == 0 && BM % 64 == 0, "fragment row bases");
-  const int arow = (wm * TM + lrow) * CH, brow = (BM + wn * TN + lrow) * CH;
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "fragment row bases");
+  const int arow = (wm * TM + lrow) * CH, brow = (wn * TN + lrow) * CH;
   const int sw = swz_key(lrow);
   const int apar = (wm * (TM / 32)) & 1, bpar = (wn * (TN / 32)) & 1;
   uint4 af[2][FM], bfr[2][FN];
-  // Read k of a chunk: 0 -> A block 0, 1..FN -> B blocks, then A blocks 1..FM-1, the order
-  // in which the chunk's MFMAs (i outer, j inner) first need them.
-  auto read_item = [&](int stage_idx, auto Cc, auto Slot, auto K) {
+  // Read k of a chunk from the A tile at a_base and the B tile at b_base: 0 -> A block 0,
+  // 1..FN -> B blocks, then A blocks 1..FM-1, the order in which the chunk's MFMAs (i
+  // outer, j inner) first need them.
+  auto read_item = [&](int a_base, int b_base, auto Cc, auto Slot, auto K) {
     constexpr int c = decltype(Cc)::value, slot = decltype(Slot)::value;
     constexpr int k = decltype(K)::value;
     constexpr bool is_a = k == 0 || k > FN;
     constexpr int idx = k == 0 ? 0 : (k <= FN ? k - 1 : k - FN);
     const int ch = ((2 * c + lhalf) ^ sw) ^ (((idx + (is_a ? apar : bpar)) & 1) * 4);
     if constexpr (is_a)
-      af[slot][idx] = lds[stage_idx + arow + idx * 32 * CH + ch];
+      af[slot][idx] = lds[a_base + arow + idx * 32 * CH + ch];
     else
-      bfr[slot][idx] = lds[stage_idx + brow + idx * 32 * CH + ch];
+      bfr[slot][idx] = lds[b_base + brow + idx * 32 * CH + ch];
   };
+  auto wrap = [](int x) { return x >= NSLOT ? x - NSLOT : x; };
 
-  // Prologue: slice 0 into stage 0, then the fragments of its first chunk.
-  static_for<0, ND>([&](auto U) { dma_item(0u, U); });
-  advance_src();
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // Ring: the A tile of slice s sits in slot 2s mod 5 and its B tile in slot 2s+1 mod 5.
+  // While slice s is multiplied, slices s+1 (A loaded, B loading) and the A tile of s+2
+  // (loading) occupy three more slots; the two slots of slice s-1 were freed by the
+  // barrier that ended it.  So an A tile has two slices of MFMAs to arrive, a B tile
+  // one; the B DMAs go out first in the slice.
+  // Prologue: A0, B0 and A1 into slots 0, 1, 2, then the fragments of slice 0's first
+  // chunk (loads complete in issue order, so vmcnt(AI) leaves only A1 in flight).
+  static_for<0, AI>([&](auto U) { dma_a(0u, U); });
+  advance_a();
+  static_for<0, BI>([&](auto U) { dma_b((uint32_t)SLOT * 16u, U); });
+  advance_b();
+  if (nsl > 1) {
+    static_for<0, AI>([&](auto U) { dma_a(2u * SLOT * 16u, U); });
+    advance_a();
+    if constexpr (AI == 8)
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
   __syncthreads();
-  static_for<0, NR>([&](auto K) { read_item(0, I<0>{}, I<0>{}, K); });
+  static_for<0, NR>([&](auto K) { read_item(0, SLOT, I<0>{}, I<0>{}, K); });
 
   // One slice: NCH chunks of NM MFMAs each.  The instruction order is fixed (a scheduling
   // fence after every MFMA slot) so that every non-MFMA instruction issues in the shadow
   // of a running MFMA:
   //   chunk c < NCH-1: the next chunk's NR fragment reads over the first NM/2 MFMAs;
-  //   chunks 0 and 1 (all but the last slice): the ND DMAs of slice s+1 into the other
-  //     stage, evenly spread;
-  //   last chunk: after MFMA BAR the wave waits for its DMAs and meets the others at the
-  //     barrier (slice s+1 is then in LDS and nobody reads slice s any more), and the
-  //     reads of slice s+1's first chunk go out over the remaining MFMAs.
-  auto slice = [&](int s, auto Load) {
-    constexpr bool LOAD = decltype(Load)::value;
-    const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
-    const uint32_t nxt_bytes = (uint32_t)nxt * 16u;
+  //   chunk 0 (MODE >= 1): the BI DMAs of B(s+1), evenly spread;
+  //   chunks 1 and 2 (MODE 2): the AI DMAs of A(s+2), evenly spread;
+  //   last chunk (MODE >= 1): after MFMA BAR the wave waits for its DMAs of A(s+1) and
+  //     B(s+1) (not those of A(s+2)) and meets the others at the barrier (slice s+1 is
+  //     then in LDS and nobody reads slice s any more), and the reads of slice s+1's
+  //     first chunk go out over the remaining MFMAs.
+  // MODE 2: slices with an A(s+2); 1: the second-to-last slice; 0: the last.
+  int sa = 0;                                  // ring slot of the current A tile
+  auto slice = [&](auto Mode) {
+    constexpr int MODE = decltype(Mode)::value;
+    const int a_cur = sa * SLOT, b_cur = wrap(sa + 1) * SLOT;
+    const int a_nxt = wrap(sa + 2) * SLOT, b_nxt = wrap(sa + 3) * SLOT;
+    const uint32_t b_load = (uint32_t)b_nxt * 16u;
+    const uint32_t a_load = (uint32_t)(wrap(sa + 4) * SLOT) * 16u;
     static_for<0, NCH>([&](auto Cc) {
       constexpr int c = decltype(Cc)::value;
       constexpr int slot = c & 1;
@@ -290,32 +323,45 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
         if constexpr (c + 1 < NCH) {
           static_for<0, NR>([&](auto K) {
             if constexpr (spread_slot(decltype(K)::value, NR, 0, NM / 2) == t)
-              read_item(cur, I<c + 1>{}, I<slot ^ 1>{}, K);
+              read_item(a_cur, b_cur, I<c + 1>{}, I<slot ^ 1>{}, K);
           });
         }
-        if constexpr (LOAD && c < DCH) {
-          static_for<0, ND>([&](auto U) {
-            if constexpr (spread_slot(decltype(U)::value, ND, 0, DCH * NM) == c * NM + t)
-              dma_item(nxt_bytes, U);
+        if constexpr (MODE >= 1 && c == 0) {
+          static_for<0, BI>([&](auto U) {
+            if constexpr (spread_slot(decltype(U)::value, BI, 0, NM) == t) dma_b(b_load, U);
           });
+          if constexpr (t == NM - 1) advance_b();
         }
-        if constexpr (LOAD && c + 1 == NCH) {
+        if constexpr (MODE == 2 && (c == 1 || c == 2)) {
+          static_for<0, AI>([&](auto U) {
+            if constexpr (spread_slot(decltype(U)::value, AI, NM, 3 * NM) == c * NM + t)
+              dma_a(a_load, U);
+          });
+          if constexpr (c == 2 && t == NM - 1) advance_a();
+        }
+        if constexpr (MODE >= 1 && c + 1 == NCH) {
           if constexpr (t == BAR) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if constexpr (MODE == 1)
+              asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            else if constexpr (AI == 8)
+              asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+            else
+              asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
             __syncthreads();
           }
           static_for<0, NR>([&](auto K) {
             if constexpr (spread_slot(decltype(K)::value, NR, BAR, NM) == t)
-              read_item(nxt, I<0>{}, I<slot ^ 1>{}, K);
+              read_item(a_nxt, b_nxt, I<0>{}, I<slot ^ 1>{}, K);
           });
         }
         __builtin_amdgcn_sched_barrier(0);
       });
     });
-    if constexpr (LOAD) advance_src();
+    sa = wrap(sa + 2);
   };
-  for (int s = 0; s + 1 < nsl; ++s) slice(s, std::true_type{});
-  slice(nsl - 1, std::false_type{});
+  for (int s = 0; s + 2 < nsl; ++s) slice(I<2>{});
+  if (nsl >= 2) slice(I<1>{});
+  slice(I<0>{});
   __syncthreads();
 
   // ---- epilogue.  Each wave stages one 32-row block of its tile at a time through its

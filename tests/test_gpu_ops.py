@@ -96,9 +96,11 @@ GEMM_SHAPES = [  # (M, N, K, batch)
 
 
 # Shapes of at least 512 256 x 256 tiles, which select the large-tile configuration of
-# 16-bit operands: ragged M and N edges, and the shortest K (one 64-element slice, so the
-# double-buffered ring runs only its prologue and last slice).
-GEMM_BIG_SHAPES = [(2000, 1100, 320, 15), (1024, 1024, 64, 32)]
+# 16-bit operands: ragged M and N edges, and the shortest K values (one, two and three
+# 64-element slices: the operand ring's prologue alone, then with its second-to-last
+# slice, then with one slice that loads two ahead).
+GEMM_BIG_SHAPES = [(2000, 1100, 320, 15), (1024, 1024, 64, 32), (1024, 1024, 128, 32),
+                   (1024, 1024, 192, 32)]
 # a few rows (decode steps): 16-column tiles, the reduction split over 4 waves in blocks of
 # 8 steps of 32 k plus a remainder, 1, 2 or 4 blocks of 16 rows
 GEMM_SKINNY_SHAPES = [(1, 2048, 8192, 2), (5, 1000, 2048, 3), (16, 4096, 2048, 1),
