@@ -47,23 +47,25 @@ struct GemmParams {
   int tiles_m, tiles_n, batch;
 };
 
-// GELU(v) = v/2 (1 + erf(v / sqrt 2)) with erf from Abramowitz & Stegun, Handbook of
-// Mathematical Functions, formula 7.1.26: for x >= 0,
-//   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),  t = 1 / (1 + p x),
-// |error| <= 1.5e-7; erf is odd.  GELU only needs erf to an absolute accuracy (it enters
-// as 1 + erf), so the GELU error is below 1e-7 |v|.
+// GELU(v) = v Phi(v) with Phi the standard normal CDF.  With h = Phi(-|v|) this is
+// max(v, 0) - |v| h for either sign of v (v >= 0: v (1 - h); v < 0: v h).  h =
+// erfc(x) / 2 at x = |v| / sqrt 2, from Abramowitz & Stegun, Handbook of Mathematical
+// Functions, formula 7.1.26: for x >= 0,
+//   erfc(x) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),  t = 1 / (1 + p x),
+// within 1.5e-7 absolute, so the GELU error is below 1e-7 |v|.  The halving is folded
+// into the coefficients and exp(-x^2) = exp2(-v^2 log2(e) / 2): eleven VALU operations
+// and two transcendentals per value.
 __device__ __forceinline__ float gelu_erf(float v) {
-  const float x = fabsf(v) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * x);
-  float poly = 1.061405429f;
-  poly = poly * t - 1.453152027f;
-  poly = poly * t + 1.421413741f;
-  poly = poly * t - 0.284496736f;
-  poly = poly * t + 0.254829592f;
+  const float a = fabsf(v);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, a, 1.0f));
+  float poly = 0.5f * 1.061405429f;
+  poly = fmaf(poly, t, 0.5f * -1.453152027f);
+  poly = fmaf(poly, t, 0.5f * 1.421413741f);
+  poly = fmaf(poly, t, 0.5f * -0.284496736f);
+  poly = fmaf(poly, t, 0.5f * 0.254829592f);
   poly *= t;
-  const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
-  const float erf_abs = 1.0f - poly * e;
-  return 0.5f * v * (1.0f + copysignf(erf_abs, v));
+  const float e = __builtin_amdgcn_exp2f(v * (v * -0.72134752044448170f));
+  return fmaf(-a, poly * e, fmaxf(v, 0.0f));
 }
 
 template <typename S>
@@ -174,6 +176,18 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int lrow = lane & 31, lhalf = lane >> 5;
+
+  // The epilogue's bias: one value per thread (tile column n0 + tid, or tile row m0 + tid
+  // for the row bias), loaded before the main loop so that its latency is hidden there,
+  // and parked in LDS once the loop is done.  (Loaded inside the epilogue, every load
+  // would wait for the memory pipe, including the stores already issued.)
+  constexpr int NB = (EPI == EPI_BIAS_M) ? BM : BN;
+  float bias_v = 0.f;
+  {
+    const int idx = (EPI == EPI_BIAS_M ? m0 : n0) + tid;
+    const int lim = EPI == EPI_BIAS_M ? p.M : p.N;
+    if (p.bias && tid < NB && idx < lim) bias_v = p.bias[z * p.sBias + idx];
+  }
 
   const S* Az = static_cast<const S*>(p.A) + z * p.sA;
   const S* Bz = static_cast<const S*>(p.B) + z * p.sB;
@@ -363,6 +377,10 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   if (nsl >= 2) slice(I<1>{});
   slice(I<0>{});
   __syncthreads();
+  // bias table: the last NB floats of LDS, clear of the epilogue's staging rows
+  float* const btab = reinterpret_cast<float*>(lds) + (NSLOT * SLOT * 4 - NB);
+  if (tid < NB) btab[tid] = bias_v;
+  __syncthreads();
 
   // ---- epilogue.  Each wave stages one 32-row block of its tile at a time through its
   // own quarter of the (now idle) LDS ring: the MFMA layout (lane = column, 16 rows per
@@ -377,10 +395,12 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   constexpr int QN = 32 * TN / 256;                    // 4-column segments per lane per block
   static_assert(32 * RS * 4 * 4 <= (int)sizeof(lds), "epilogue staging exceeds LDS");
   float* stage = reinterpret_cast<float*>(lds) + wave * 32 * RS;
-  const float* biasz = p.bias ? p.bias + z * p.sBias : nullptr;
+  static_assert(4 * 32 * RS <= NSLOT * SLOT * 4 - NB, "staging rows overlap the bias table");
   const float* Rz = p.R ? p.R + z * p.sR : nullptr;
   OutT* Cz = static_cast<OutT*>(p.C) + z * p.sC;
   const bool vec_ok = (p.ldc & 3) == 0;
+  // the whole tile inside C, with 16-byte-aligned row segments (uniform per workgroup)
+  const bool interior = vec_ok && m0 + BM <= p.M && n0 + BN <= p.N;
   const int rows0 = m0 + wm * TM, cols0 = n0 + wn * TN;
   // segment q of block i: row ml, columns nl .. nl + 3 of the wave's sub-tile
   auto seg_ml = [&](int q) { return (q * 64 + lane) / (TN / 4); };
@@ -401,14 +421,15 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
     load_res(0, rbuf[0]);
     load_res(1, rbuf[1]);
   }
+  float bnj[FN];                                       // column bias of the lane's columns
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bnj[j] = (EPI != EPI_BIAS_M) ? btab[wn * TN + j * 32 + lrow] : 0.f;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int nl = j * 32 + lrow;
-      float bn = 0.f;
-      if constexpr (EPI != EPI_BIAS_M)
-        bn = (biasz && cols0 + nl < p.N) ? biasz[cols0 + nl] : 0.f;
+      const float bn = bnj[j];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ml = (r >> 2) * 8 + lhalf * 4 + (r & 3);
@@ -419,6 +440,38 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
+    if (interior) {
+      // No edge checks: each half block's QH staged segments are read back to back, so
+      // the LDS latency is paid once per half block rather than once per segment.
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        if constexpr (EPI == EPI_BIAS_N_RES) {
+          if (hb == 1 && 2 * i + 2 < 2 * FM) load_res(2 * i + 2, rbuf[0]);
+        }
+        float4 vq[QH];
+        float bmq[QH];
+#pragma unroll
+        for (int qq = 0; qq < QH; ++qq) {
+          const int q = hb * QH + qq;
+          vq[qq] = *reinterpret_cast<const float4*>(stage + seg_ml(q) * RS + seg_nl(q));
+          if constexpr (EPI == EPI_BIAS_M) bmq[qq] = btab[wm * TM + i * 32 + seg_ml(q)];
+        }
+#pragma unroll
+        for (int qq = 0; qq < QH; ++qq) {
+          const int q = hb * QH + qq;
+          float4 v = vq[qq];
+          if constexpr (EPI == EPI_BIAS_M) {
+            v.x += bmq[qq]; v.y += bmq[qq]; v.z += bmq[qq]; v.w += bmq[qq];
+          }
+          if constexpr (EPI == EPI_BIAS_N_RES) {
+            const float4 rr = rbuf[hb][qq];
+            v.x += rr.x; v.y += rr.y; v.z += rr.z; v.w += rr.w;
+          }
+          const int m = rows0 + i * 32 + seg_ml(q), n = cols0 + seg_nl(q);
+          store4<OutT>(Cz + (int64_t)m * p.ldc + n, v);
+        }
+      }
+    } else {
 #pragma unroll
     for (int q = 0; q < QN; ++q) {
       if constexpr (EPI == EPI_BIAS_N_RES) {
@@ -430,7 +483,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
       if (m >= p.M) continue;
       float4 v = *reinterpret_cast<const float4*>(stage + ml * RS + nl);
       if constexpr (EPI == EPI_BIAS_M) {
-        const float bm = biasz ? biasz[m] : 0.f;
+        const float bm = btab[wm * TM + i * 32 + ml];
         v.x += bm; v.y += bm; v.z += bm; v.w += bm;
       }
       OutT* dst = Cz + (int64_t)m * p.ldc + n;
@@ -452,6 +505,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
           store_val<OutT>(dst + k, o);
         }
       }
+    }
     }
     if constexpr (EPI == EPI_BIAS_N_RES) {
       if (2 * i + 3 < 2 * FM) load_res(2 * i + 3, rbuf[1]);

@@ -170,6 +170,32 @@ def test_gemm_without_bias_or_residual():
     check_close(f64(C), f64(A) @ f64(B).T, "f32", "gemm plain", rel_elem=1e-5, rel_rms=1e-5)
 
 
+def test_gemm_gelu_epilogue_accuracy():
+    """The GELU epilogue alone: an fp32 GEMM whose products are exactly v (one nonzero k)
+    feeds a grid of arguments to it, and the result must stay within twice the
+    approximation's absolute error of 1e-7 |v| (plus fp32 rounding of the few operations and
+    of the hardware reciprocal and exp2) of the exact erf form, for both signs and far into
+    either tail."""
+    M, N, Kd = 4096, 64, 64
+    v = np.concatenate([np.linspace(-12.0, 12.0, M - 6), [0.0, -0.0, 1e-30, -1e-30, 40.0, -40.0]])
+    A = torch.zeros((M, Kd), dtype=torch.float32)
+    A[:, 0] = torch.from_numpy(v).float()
+    B = torch.zeros((N, Kd), dtype=torch.float32)
+    B[:, 0] = 1.0
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    K().op_gemm(1, A.to(DEV), B.to(DEV), C, None, None, M, N, Kd, 1, 0, 0, 0, 0)
+    torch.cuda.synchronize()
+    x = f64(A[:, 0])                                   # the fp32 arguments
+    ref = np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in x])
+    got = f64(C)
+    bound = 2e-7 * np.abs(x) + 8 * 2.0 ** -24 * np.abs(ref) + 1e-37
+    err = np.abs(got - ref[:, None])
+    assert np.all(np.isfinite(got))
+    assert np.all(err <= bound[:, None]), (float(np.max(err / bound[:, None])),
+                                           x[np.argmax(np.max(err, axis=1) / bound)])
+    assert np.all(got[x == 0.0] == 0.0)
+
+
 def test_gemm_shared_residual_batch_stride_zero():
     M, N, Kd, batch = 50, 64, 64, 3
     g = torch.Generator(device="cpu").manual_seed(4)
