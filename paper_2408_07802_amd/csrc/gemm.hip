@@ -20,9 +20,9 @@
 // MFMAs to arrive and B tiles one.  Tile rows are 128 bytes; 16-byte chunk c of row r
 // is stored at chunk c ^ swz_key(r), which keeps fragment reads free of bank conflicts.
 // The swizzle is applied on the load side: each lane of a DMA load writes the next 16
-// bytes of LDS, so it fetches the logical chunk that belongs there.  The main loop's instruction order is fixed by
-// hand (fragment reads and DMAs interleaved one per MFMA, one barrier per slice) so
-// that the single wave per SIMD keeps the matrix pipe busy.
+// bytes of LDS, so it fetches the logical chunk that belongs there.  The main loop's
+// instruction order is fixed by hand (fragment reads and DMAs interleaved one per MFMA,
+// one barrier per slice) so that the single wave per SIMD keeps the matrix pipe busy.
 // Rows past M (or N) load a clamped in-bounds row; they only feed outputs that
 // are never stored.
 #include <type_traits>
@@ -127,9 +127,9 @@ typedef __attribute__((address_space(3))) void* lds_void_ptr;
 // One 16-byte-per-lane DMA from global memory into LDS: global_load_lds_dwordx4 with a
 // wave-uniform base address (SGPR pair), a per-lane 32-bit byte offset, and the
 // wave-uniform LDS destination in M0; lane i's 16 bytes land at M0 + 16 i.  It is issued
-// from inline assembly so that the compiler does not order later LDS reads of the *other*
-// stage behind it; the kernel orders it explicitly (s_waitcnt vmcnt(0) + barrier before
-// the stage is read).
+// from inline assembly so that the compiler does not order later LDS reads of *other*
+// ring slots behind it; the kernel orders it explicitly (s_waitcnt vmcnt + barrier before
+// the slot is read).
 __device__ __forceinline__ void dma16(uint32_t lds_addr, const void* base, uint32_t off) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                :: "s"(lds_addr), "v"(off), "s"(base) : "memory", "m0");
