@@ -49,8 +49,8 @@ TRAFFIC = {
     # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
-        "source_sha256": "564f175073ad8eefec4253b8fc667047f5d002575c80336db6b863d098bb3640",
-        "read_bytes": 3508879613, "write_bytes": 1073832530,
+        "source_sha256": "631a0a323366276a9d18fa313728a12d3b544397f2e948b6a5ede4f5550aea59",
+        "read_bytes": 3472554482, "write_bytes": 1073875504,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
