@@ -60,13 +60,13 @@ __device__ __forceinline__ void store4<f16>(f16* dst, float a, float b, float c,
   *reinterpret_cast<f16x4*>(dst) = v;
 }
 
-// Normalise v (this thread's float4s of one row) and write the row to dst.
-template <typename S>
+// Normalise v (this thread's float4s of one row, at most V) and write the row to dst.
+template <typename S, int V>
 __device__ __forceinline__ void ln_write(const float4* v, int nv, float mean, float rstd,
                                          const float* gamma, const float* beta, S* dst) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int u = 0; u < MAX_VEC; ++u) {
+  for (int u = 0; u < V; ++u) {
     if (u >= nv) break;
     const int c = (tid + u * NORM_THREADS) * 4;
     const float4 g = *reinterpret_cast<const float4*>(gamma + c);
@@ -76,22 +76,30 @@ __device__ __forceinline__ void ln_write(const float4* v, int nv, float mean, fl
   }
 }
 
+template <int V>
 __device__ __forceinline__ void row_stats(const float4* v, int nv, int d, float eps,
                                           float* red, float& mean, float& rstd) {
   float s = 0.f;
 #pragma unroll
-  for (int u = 0; u < MAX_VEC; ++u)
+  for (int u = 0; u < V; ++u)
     if (u < nv) s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
   mean = block_sum(s, red) / (float)d;
   float q = 0.f;
 #pragma unroll
-  for (int u = 0; u < MAX_VEC; ++u)
+  for (int u = 0; u < V; ++u)
     if (u < nv) {
       const float a = v[u].x - mean, b = v[u].y - mean, c = v[u].z - mean, e = v[u].w - mean;
       q += (a * a + b * b) + (c * c + e * e);
     }
   const float var = block_sum(q, red) / (float)d;
   rstd = rsqrtf(var + eps);
+}
+
+// Float4s per thread a row of d floats needs at most (1, 2, 4 or MAX_VEC): the kernels'
+// register arrays are sized by it, so a short row keeps occupancy high.
+inline int vecs_for(int d) {
+  const int v = (d / 4 + NORM_THREADS - 1) / NORM_THREADS;
+  return v <= 1 ? 1 : v <= 2 ? 2 : v <= 4 ? 4 : MAX_VEC;
 }
 
 // Number of float4s this thread owns in a row of d floats.
@@ -101,7 +109,8 @@ __device__ __forceinline__ int my_vecs(int d) {
   return tid < nv4 ? (nv4 - tid + NORM_THREADS - 1) / NORM_THREADS : 0;
 }
 
-template <typename S>
+// V: float4s per thread that the launch's d needs at most (registers are sized by it).
+template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
     const float* __restrict__ x, int64_t xs, const float* __restrict__ gamma,
     const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, float eps) {
@@ -111,22 +120,22 @@ __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
   // sub-layers [i0, i1) of this block (gridDim.y blocks share the n sub-layers)
   const int i0 = (int)((int64_t)n * blockIdx.y / gridDim.y);
   const int i1 = (int)((int64_t)n * (blockIdx.y + 1) / gridDim.y);
-  float4 v[MAX_VEC];
+  float4 v[V];
   float mean = 0.f, rstd = 0.f;
   for (int i = i0; i < i1; ++i) {
     if (i == i0 || xs != 0) {
       const float* row = x + i * xs + (int64_t)t * d;
 #pragma unroll
-      for (int u = 0; u < MAX_VEC; ++u)
+      for (int u = 0; u < V; ++u)
         if (u < nv) v[u] = *reinterpret_cast<const float4*>(row + (threadIdx.x + u * NORM_THREADS) * 4);
-      row_stats(v, nv, d, eps, red, mean, rstd);
+      row_stats<V>(v, nv, d, eps, red, mean, rstd);
     }
-    ln_write(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
+    ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
              out + ((int64_t)i * T + t) * d);
   }
 }
 
-template <typename S>
+template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
     const float* __restrict__ x, const float* __restrict__ shared, const float* __restrict__ h,
     const float* __restrict__ gamma, const float* __restrict__ beta, S* __restrict__ out, int n,
@@ -135,10 +144,10 @@ __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
   const int t = blockIdx.x;
   const int nv = my_vecs(d);
   const int64_t plane = (int64_t)T * d;
-  float4 y[MAX_VEC];
+  float4 y[V];
   // y = X (first layer) or the N-way sum of the previous layer's outputs
 #pragma unroll
-  for (int u = 0; u < MAX_VEC; ++u) {
+  for (int u = 0; u < V; ++u) {
     if (u >= nv) break;
     const int c = (threadIdx.x + u * NORM_THREADS) * 4;
     if (shared) {
@@ -155,18 +164,18 @@ __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
   const int i0 = (int)((int64_t)n * blockIdx.y / gridDim.y);
   const int i1 = (int)((int64_t)n * (blockIdx.y + 1) / gridDim.y);
   for (int i = i0; i < i1; ++i) {
-    float4 v[MAX_VEC];
+    float4 v[V];
     const float* hrow = h + i * plane + (int64_t)t * d;
 #pragma unroll
-    for (int u = 0; u < MAX_VEC; ++u) {
+    for (int u = 0; u < V; ++u) {
       if (u >= nv) break;
       const float4 a = *reinterpret_cast<const float4*>(hrow + (threadIdx.x + u * NORM_THREADS) * 4);
       v[u] = make_float4(a.x + y[u].x, a.y + y[u].y, a.z + y[u].z, a.w + y[u].w);
     }
     float mean, rstd;
-    row_stats(v, nv, d, eps, red, mean, rstd);
-    ln_write(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
-             out + (i * plane + (int64_t)t * d));
+    row_stats<V>(v, nv, d, eps, red, mean, rstd);
+    ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
+                   out + (i * plane + (int64_t)t * d));
   }
 }
 
@@ -255,9 +264,14 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
-    hipLaunchKernelGGL(layernorm_kernel<S>, dim3(T, sub_groups(n, T)), dim3(NORM_THREADS), 0, s,
-                       x, xs, gamma, beta,
-                       static_cast<S*>(out), n, T, d, eps);
+    const dim3 grid(T, sub_groups(n, T)), block(NORM_THREADS);
+    S* o = static_cast<S*>(out);
+    switch (vecs_for(d)) {
+      case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
+      case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
+      case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
+      default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
+    }
     return hipGetLastError();
   });
 }
@@ -269,9 +283,14 @@ hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, con
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
-    hipLaunchKernelGGL(combine_ln2_kernel<S>, dim3(T, sub_groups(n, T)), dim3(NORM_THREADS), 0, s,
-                       x, shared, h,
-                       gamma, beta, static_cast<S*>(out), n, T, d, eps);
+    const dim3 grid(T, sub_groups(n, T)), block(NORM_THREADS);
+    S* o = static_cast<S*>(out);
+    switch (vecs_for(d)) {
+      case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
+      case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
+      case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
+      default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
+    }
     return hipGetLastError();
   });
 }
