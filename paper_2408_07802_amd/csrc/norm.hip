@@ -264,7 +264,9 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
-    const dim3 grid(T, sub_groups(n, T)), block(NORM_THREADS);
+    // one workgroup per (token, sub-layer) row when the rows differ (more rows in flight);
+    // a shared input row keeps its statistics in one workgroup per token
+    const dim3 grid(T, xs != 0 ? (unsigned)n : sub_groups(n, T)), block(NORM_THREADS);
     S* o = static_cast<S*>(out);
     switch (vecs_for(d)) {
       case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
