@@ -47,7 +47,8 @@ struct AttnParams {
   int n, T, d, n_heads, ldv, num_seqs;
   int dkv, group;         // key/value width, query heads per key/value head
   int head_group;         // heads per XCD group of the workgroup order (0: plain order)
-  float scale_log2;       // log2(e) / sqrt(hd)
+  float scale_log2;       // log2(e) / sqrt(hd), or 1 when Q already carries that factor
+  int q_prescaled;        // Q columns were multiplied by log2(e) / sqrt(hd) upstream
   int cu[KRAKEN_MAX_SEQS + 1];
   int tile_prefix[KRAKEN_MAX_SEQS + 1];
 };
@@ -476,7 +477,12 @@ __device__ __forceinline__ float sum8<bf16>(uint4 v, float acc) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, v.w), one, acc, false);
 }
 
-template <typename S, int HD>
+// PRE: Q already carries log2(e) / sqrt(hd), so the scores come out of the MFMAs in log2
+// units.  Then the first S MFMAs of a tile accumulate onto -c0 (a per-lane constant: in the
+// transposed layout a lane's 16 score registers all belong to its query), c0 being the
+// running maximum, and a weight is a bare exp2 of its accumulator; only a rescale (rare)
+// shifts the tile's scores by the growth of the maximum.
+template <typename S, int HD, bool PRE>
 __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   constexpr int NW = 8, QW = 32;
   constexpr int EPC = 8;                      // 16-bit elements per 16-byte chunk
@@ -645,6 +651,8 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     for (int r = 0; r < 16; ++r) oacc[ob][r] = 0.f;
   float m_run = -1e30f, l_run = 0.f;
   const float scale = p.scale_log2;
+  float c0 = 0.f;                             // (PRE) the S accumulators start from -c0
+  f32x16 cneg = {};
   f32x16 sacc[2];                             // S(t), key blocks 0 and 1
   uint4 pb[2][2];                             // 16-bit P(t-1): [key block][half]
 #pragma unroll
@@ -675,7 +683,8 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
         oacc[ob] = mfma_chunk<S>(vf[j % RING], pb[sb][hh], oacc[ob]);
         if constexpr (j + RING < NP) vf[j % RING] = v_frag(vst, j + RING);
       } else {
-        sacc[j & 1] = mfma_chunk<S>(kf[j % RING], qf[j >> 1], j < 2 ? zero16 : sacc[j & 1]);
+        sacc[j & 1] = mfma_chunk<S>(kf[j % RING], qf[j >> 1],
+                                    j < 2 ? (PRE ? cneg : zero16) : sacc[j & 1]);
         if constexpr (j + RING < NS) kf[j % RING] = k_frag(kst, j + RING);
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -711,7 +720,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
       for (int r = 2; r < 8; r += 2) mq[q] = fmaxf(fmaxf(mq[q], sq[o + r]), sq[o + r + 1]);
     }
     const float mraw = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-    float mx = fmaxf(m_run, mraw * scale);
+    float mx = fmaxf(m_run, PRE ? mraw + c0 : mraw * scale);
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
                                                      false, false);
     mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
@@ -724,6 +733,16 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
       for (int ob = 0; ob < OB; ++ob)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[ob][r] *= alpha;
+      if constexpr (PRE) {
+        const float shift = mx - c0;
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sacc[sb][r] -= shift;
+        c0 = mx;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cneg[r] = -mx;
+      }
       m_run = mx;
     }
     // weights, packed to 16 bits for the PV MFMAs; the row sum adds the packed (rounded)
@@ -733,7 +752,8 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        sacc[sb][r] = __builtin_amdgcn_exp2f(fmaf(sacc[sb][r], scale, -m_run));
+        sacc[sb][r] = PRE ? __builtin_amdgcn_exp2f(sacc[sb][r])
+                          : __builtin_amdgcn_exp2f(fmaf(sacc[sb][r], scale, -m_run));
       typedef S s8 __attribute__((ext_vector_type(8)));
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
@@ -817,9 +837,12 @@ template <typename S, int HD>
 void launch_hd(const AttnParams& p, dim3 grid, hipStream_t s) {
   constexpr int NQB = nqb_for<S, HD>();
   // (the ping-pong form needs enough MFMA work per tile to cover the softmax: head size 128)
-  if constexpr (sizeof(S) == 2 && HD == 128)
-    hipLaunchKernelGGL((attn_pp_kernel<S, HD>), grid, dim3(512), 0, s, p);
-  else
+  if constexpr (sizeof(S) == 2 && HD == 128) {
+    if (p.q_prescaled)
+      hipLaunchKernelGGL((attn_pp_kernel<S, HD, true>), grid, dim3(512), 0, s, p);
+    else
+      hipLaunchKernelGGL((attn_pp_kernel<S, HD, false>), grid, dim3(512), 0, s, p);
+  } else
     hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
 }
 
@@ -849,7 +872,9 @@ hipError_t launch_attention(const AttnDesc& a, hipStream_t s) {
   if (a.n_heads % kvh != 0) return hipErrorInvalidValue;
   p.dkv = kvh * hd;
   p.group = a.n_heads / kvh;
-  p.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
+  p.q_prescaled = a.q_prescaled ? 1 : 0;
+  p.scale_log2 =
+      a.q_prescaled ? 1.0f : (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
   p.tile_prefix[0] = 0;
   for (int b = 0; b <= a.num_seqs; ++b) p.cu[b] = a.cu_host[b];
   for (int b = 0; b < a.num_seqs; ++b)

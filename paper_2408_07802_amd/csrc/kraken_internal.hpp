@@ -88,6 +88,7 @@ struct AttnDesc {
   int n, T, d, n_heads, n_kv_heads;
   const int32_t* cu_host;  // host cu_seqlens [num_seqs + 1]
   int num_seqs;
+  int q_prescaled;          // the Q columns already carry log2(e) / sqrt(hd)
 };
 
 hipError_t launch_attention(const AttnDesc& a, hipStream_t s);
@@ -142,9 +143,13 @@ int64_t decode_partial_floats(int n, int B, int n_heads, int hd, int splits);
 // out [n][B][d] = attention of the Q columns of qk [n][B][d + dkv] over keys
 // 0..lens_host[b] of slot b (the new token's own included, already appended).  part: fp32
 // scratch of part_floats elements; the key range is split into as many chunks as it holds.
+// q_prescaled: the Q columns already carry log2(e) / sqrt(hd).
 hipError_t launch_decode_attention(DType dt, const void* qk, const void* cache_layer,
                                    float* part, int64_t part_floats, void* out, int n, int B,
                                    int d, int n_heads, int n_kv_heads, const int32_t* lens_host,
-                                   int max_seqs, int capacity, hipStream_t s);
+                                   int max_seqs, int capacity, int q_prescaled, hipStream_t s);
+
+// p[k] *= c for k < count (operand type dt).
+hipError_t launch_scale(DType dt, void* p, int64_t count, float c, hipStream_t s);
 
 }  // namespace kraken

@@ -187,6 +187,13 @@ __global__ void to_f32_kernel(const S* __restrict__ src, float* __restrict__ dst
 }
 
 template <typename S>
+__global__ void scale_kernel(S* __restrict__ p, int64_t count, float c) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < count; k += stride)
+    p[k] = (S)((float)p[k] * c);
+}
+
+template <typename S>
 __global__ void split16_kernel(const float* __restrict__ src, S* __restrict__ dst, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < count; k += stride) {
@@ -293,6 +300,16 @@ hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, con
       case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
       default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
     }
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_scale(DType dt, void* p, int64_t count, float c, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(scale_kernel<S>, dim3(grid_for(count)), dim3(256), 0, s,
+                       static_cast<S*>(p), count, c);
     return hipGetLastError();
   });
 }

@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -282,6 +283,14 @@ hipError_t repack_sub(kraken_model* m, int j, int i, const void* src, hipStream_
   R_(launch_transpose(st, cptr(src, so.Wqkv, st), wq, dt,
                       static_cast<char*>(w.WqkT) + i * (d + dkv) * d * es, d, (int)d,
                       (int)(d + dkv), of, s));
+  // The Q projection (the first d rows of WqkT, the first d biases) carries the softmax
+  // factor log2(e) / sqrt(hd), so the attention kernels get scores in log2 units straight
+  // from their MFMAs.
+  {
+    const float qs = (float)(1.4426950408889634 / std::sqrt((double)(d / m->H)));
+    R_(launch_scale(dt, static_cast<char*>(w.WqkT) + i * (d + dkv) * d * es, d * d, qs, s));
+    R_(launch_scale(DType::F32, w.bqk + i * (d + dkv), d, qs, s));
+  }
   R_(launch_transpose(st, cptr(src, so.Wqkv + d + dkv, st), wq, dt,
                       static_cast<char*>(w.WvT) + i * dkv * d * es, d, (int)d, (int)dkv, of, s));
   R_(launch_transpose(st, cptr(src, so.Wo, st), d, dt, static_cast<char*>(w.WoT) + i * d * d * es,
@@ -391,6 +400,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
       a.dt = dt; a.qk = m->qk; a.vt = m->vt; a.out = m->o;
       a.n = (int)N; a.T = T; a.d = (int)d; a.n_heads = m->H; a.n_kv_heads = m->Hkv;
       a.cu_host = cu; a.num_seqs = num_seqs;
+      a.q_prescaled = 1;
       RUN(KRAKEN_K_ATTN, launch_attention(a, s), "attention");
     } else {
       // V rows of the new tokens go through o ([N][T][dkv]) into the cache; o then takes
@@ -412,7 +422,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
       RUN(KRAKEN_K_ATTN,
           launch_decode_attention(dt, m->qk, cache_j, static_cast<float*>(m->vt),
                                   decode_partial_room(m), m->o, (int)N, T, (int)d, m->H,
-                                  m->Hkv, kv->lens, kv->max_seqs, kv->cap, s),
+                                  m->Hkv, kv->lens, kv->max_seqs, kv->cap, 1, s),
           "decode attention");
     }
     {
@@ -897,6 +907,7 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
   a.dt = (DType)dtype; a.qk = qk; a.vt = vt; a.out = out;
   a.n = n; a.T = (int)T; a.d = d; a.n_heads = n_heads; a.n_kv_heads = n_kv_heads;
   a.cu_host = cu_seqlens; a.num_seqs = num_seqs;
+  a.q_prescaled = 0;
   hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "attention");
 }
@@ -928,7 +939,7 @@ kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const vo
     return fail(KRAKEN_ERR_INVALID_ARG, "work is smaller than n * B * n_heads * (hd + 2)");
   hipError_t e = launch_decode_attention((DType)dtype, qk, kv_layer, work, work_floats, out, n,
                                          num_seqs, d, n_heads, n_kv_heads, lens, max_seqs,
-                                         capacity, static_cast<hipStream_t>(stream));
+                                         capacity, 0, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "decode attention");
 }
 
