@@ -141,7 +141,7 @@ struct DecAttnParams {
   const void* cache;
   float* part;      // [n][B][H][S][hd + 2]: max, sum, unnormalised output
   int n, B, d, dkv, H, Hkv, group, max_seqs, cap, S, chunk;
-  float scale_log2; // log2(e) / sqrt(hd), or 1 when Q already carries it (scores in log2 units)
+  float scale;      // 1 / sqrt(hd); ln 2 when Q already carries log2(e) / sqrt(hd)
   int lens[KRAKEN_MAX_SEQS];   // cached tokens of slot b, new token included at lens[b]
 };
 
@@ -281,20 +281,20 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecAttnParams p) {
 #pragma unroll
       for (int j = 0; j < R; ++j) {
         // the row's full dot product, in every lane of its group
-        const float a = group_sum<LPR>(chunk_dot<S>(kr[j], q[g])) * p.scale_log2;
+        const float a = group_sum<LPR>(chunk_dot<S>(kr[j], q[g])) * p.scale;
         sc[j] = kb + j * RPP + row0 < k_end ? a : -INFINITY;
         mx = fmaxf(mx, sc[j]);
       }
       mx = xor_max_from<LPR>(mx);
       const float m_new = fmaxf(m_run[g], mx);
       const float mref = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mref);
+      const float alpha = __expf(m_run[g] - mref);
       float ps = 0.f;
 #pragma unroll
       for (int u = 0; u < EPC; ++u) acc[g][u] *= alpha;
 #pragma unroll
       for (int j = 0; j < R; ++j) {
-        const float pj = __builtin_amdgcn_exp2f(sc[j] - mref);
+        const float pj = __expf(sc[j] - mref);
         ps += pj;
         const S* e = reinterpret_cast<const S*>(&vr[j]);
 #pragma unroll
@@ -327,7 +327,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecAttnParams p) {
     const float M = fmaxf(fmaxf(wm[0][g], wm[1][g]), fmaxf(wm[2][g], wm[3][g]));
     float sw[4];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) sw[w] = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(wm[w][g] - M);
+    for (int w = 0; w < 4; ++w) sw[w] = M == -INFINITY ? 0.f : __expf(wm[w][g] - M);
     for (int f = tid; f < HD; f += 256)
       out[2 + f] = (wo[0][g][f] * sw[0] + wo[1][g][f] * sw[1]) +
                    (wo[2][g][f] * sw[2] + wo[3][g][f] * sw[3]);
@@ -345,8 +345,7 @@ struct DecCombineParams {
 };
 
 // Block (sub-layer, sequence, head), one thread per output feature: the chunk partials
-// (m_s, l_s, o_s) merge as o = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max m_s
-// (scores and maxima are in log2 units).
+// (m_s, l_s, o_s) merge as o = sum_s o_s e^(m_s - M) / sum_s l_s e^(m_s - M), M = max m_s.
 template <typename S>
 __global__ __launch_bounds__(128) void decode_combine_kernel(DecCombineParams p) {
   int r = blockIdx.x;
@@ -362,7 +361,7 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(DecCombineParams p)
   for (int s = 0; s < p.S; ++s) {
     const float ms = part[s * (p.hd + 2)];
     if (ms == -INFINITY) continue;               // a chunk past the sequence's keys
-    const float w = __builtin_amdgcn_exp2f(ms - M);
+    const float w = __expf(ms - M);
     L += part[s * (p.hd + 2) + 1] * w;
     O += part[s * (p.hd + 2) + 2 + t] * w;
   }
@@ -478,7 +477,8 @@ hipError_t launch_decode_attention(DType dt, const void* qk, const void* cache_l
   p.max_seqs = max_seqs; p.cap = capacity;
   p.chunk = chunk;
   p.S = (max_keys + chunk - 1) / chunk;
-  p.scale_log2 = q_prescaled ? 1.0f : (float)(1.4426950408889634 / sqrt((double)hd));
+  // scores in natural units: a pre-scaled Q's dot products are in log2 units
+  p.scale = q_prescaled ? 0.69314718055994531f : (float)(1.0 / sqrt((double)hd));
   for (int b = 0; b < B; ++b) p.lens[b] = lens_host[b];
   hipError_t e;
   switch (dt) {
