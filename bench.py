@@ -41,8 +41,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "1b2e345a7c120ac2b18cc0e75ad6bb506a9579a5ed8b73d8740864c074bb406a",
-        "read_bytes": 3230405818, "write_bytes": 269484630,
+        "source_sha256": "d3eb1be59afbc4e1b99ade4c4629882fce94a7254e174cf7e32b2e63070b87b5",
+        "read_bytes": 3240122337, "write_bytes": 269491452,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
@@ -50,7 +50,7 @@ TRAFFIC = {
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
         "source_sha256": "631a0a323366276a9d18fa313728a12d3b544397f2e948b6a5ede4f5550aea59",
-        "read_bytes": 3472554482, "write_bytes": 1073875504,
+        "read_bytes": 3522950115, "write_bytes": 1073835592,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
@@ -58,8 +58,8 @@ TRAFFIC = {
     # kernel plus its chunk merge
     "decode_attention_b1_ctx8192": {
         "source": "paper_2408_07802_amd/csrc/decode.hip",
-        "source_sha256": "99e0f0ad725281d6d4539686de8880789824f406a41a1b9aa754bd2759fc5ad8",
-        "read_bytes": 537730065, "write_bytes": 450560,
+        "source_sha256": "df9a080c2d386a595471223a32068cc34f39fdf729f5379a6d1d5b8a6b132629",
+        "read_bytes": 537726597, "write_bytes": 450560,
         "algorithmic_bytes": 537034752,
         "profile": "profiles/hbm_traffic_decode_n8_l24_d2048_ctx8192.md",
     },
