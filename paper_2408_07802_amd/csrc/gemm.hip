@@ -759,7 +759,10 @@ hipError_t launch_gemm(const GemmDesc& g, hipStream_t s) {
   // 128 x 64 7-10% faster, 464 -> 128 x 64 40% slower).
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256) * g.batch;
   const int64_t mid = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128) * g.batch;
-  const int cfg = big >= 512 ? 2 : mid >= 256 ? 1 : 0;
+  // 256 x 256 tiles need two waves of workgroups to hide their tail, except when one
+  // tile per CU fills the chip exactly and the reduction is long (the W_concat shape)
+  const bool one_round = big == 256 && (int64_t)g.K * g.kgroups >= 8192;
+  const int cfg = (big >= 512 || one_round) ? 2 : mid >= 256 ? 1 : 0;
   switch (g.dt) {
     case DType::BF16:
       return cfg == 2 ? launch_cfg<bf16, 256, 256>(g, s)

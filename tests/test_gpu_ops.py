@@ -196,6 +196,31 @@ def test_gemm_gelu_epilogue_accuracy():
     assert np.all(got[x == 0.0] == 0.0)
 
 
+@pytest.mark.parametrize("epi", [0, 2])
+def test_gemm_one_tile_per_cu_long_k(epi):
+    """256 tiles of 256 x 256 with K = 8192: the one-round large-tile configuration (the
+    W_concat shape).  Sampled rows of every batch entry against fp64."""
+    M, N, Kd, batch = 2048, 2048, 8192, 4
+    g = torch.Generator(device="cpu").manual_seed(77 + epi)
+    A = torch.randn((batch, M, Kd), generator=g).to(torch.float16).to(DEV)
+    B = (torch.randn((batch, N, Kd), generator=g) / math.sqrt(Kd)).to(torch.float16).to(DEV)
+    bias = (0.5 * torch.randn((batch, N), generator=g)).to(DEV)
+    R = torch.randn((batch, M, N), generator=g).to(DEV) if epi == 2 else None
+    C = torch.full((batch, M, N), float("nan"),
+                   dtype=torch.float32 if epi == 2 else torch.float16, device=DEV)
+    K().op_gemm(epi, A, B, C, bias, R, M, N, Kd, batch, M * Kd, N * Kd, M * N, M * N)
+    torch.cuda.synchronize()
+    rows = torch.arange(0, M, 61)
+    for z in range(batch):
+        ref = f64(A[z, rows]) @ f64(B[z]).T + f64(bias[z])[None, :]
+        if epi == 2:
+            ref = ref + f64(R[z, rows])
+            check_close(f64(C[z, rows]), ref, "f32", f"one-round gemm {z}", rel_elem=1e-5,
+                        rel_rms=1e-5)
+        else:
+            check_close(f64(C[z, rows]), ref, "f16", f"one-round gemm {z}")
+
+
 def test_gemm_shared_residual_batch_stride_zero():
     M, N, Kd, batch = 50, 64, 64, 3
     g = torch.Generator(device="cpu").manual_seed(4)
