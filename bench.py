@@ -49,8 +49,8 @@ TRAFFIC = {
     # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
-        "source_sha256": "631a0a323366276a9d18fa313728a12d3b544397f2e948b6a5ede4f5550aea59",
-        "read_bytes": 3522950115, "write_bytes": 1073835592,
+        "source_sha256": "effd3922bb55abfeb0bc953e33b833e831c0877044923b0628aa0ef7f5d8cd97",
+        "read_bytes": 3571242872, "write_bytes": 1073882874,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
