@@ -280,7 +280,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the N sub-layers would shard across GPUs)",
+              "(over G GPUs each would own N/G complete sub-layer chains, with one all-reduce "
+              "of the partial N-way sum per layer)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -23,7 +23,7 @@ Transformers For Efficient Multi-Device Inference", arXiv 2408.07802):
   two linears with a GELU in between; LayerNorms sit before MHA and FFN
   (pre-LN).
 
-Readings where the paper is silent (each is restated in the design doc):
+Readings where the paper is silent or ambiguous:
 LayerNorm uses the biased variance and eps = 1e-5; GELU is the exact erf form;
 all four linears carry a bias, ``W_concat`` does not; the causal mask applies
 within each packed sequence only; ``y`` includes the sub-layer's own input
