@@ -279,7 +279,7 @@ def main():
                     help="run one GPU's share of a G-way split: N/G sub-layers per layer")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(over G GPUs each would own N/G complete sub-layer chains, with one all-reduce "
               "of the partial N-way sum per layer)",
               file=sys.stderr)

@@ -48,7 +48,7 @@ extern "C" {
 typedef enum {
   KRAKEN_OK = 0,
   KRAKEN_ERR_INVALID_ARG = 1,  /* a null pointer, a bad size, a bad cu_seqlens */
-  KRAKEN_ERR_UNSUPPORTED = 2,  /* a valid configuration this build does not implement */
+  KRAKEN_ERR_UNSUPPORTED = 2,  /* a valid configuration the library does not implement */
   KRAKEN_ERR_OOM = 3,          /* device allocation failed; nothing is leaked */
   KRAKEN_ERR_STATE = 4,        /* e.g. kraken_prefill before kraken_load_weights */
   KRAKEN_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed */
