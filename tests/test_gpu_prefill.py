@@ -276,6 +276,32 @@ def test_host_blob_load_matches_device_blob_load():
     m2.close()
 
 
+def test_reloading_weights_gives_the_same_model():
+    """Loading the same blob twice (and loading another blob in between) leaves the model
+    exactly as one load does: the repack derives every internal operand (including the Q
+    projection, which carries the softmax factor) from the blob, never from the previous
+    contents.  Head size 128 in fp16 takes the ping-pong attention form."""
+    w = small("reload", n_sub=2, n_layers=2, d_model=256, n_heads=2, d_ff=512, compute="f16")
+    T = 130
+    cfg = cfg_of(w, T)
+    blob = K().pack_weights((synth.gen_layer(w, j, 0, DEV, "random") for j in range(2)),
+                            synth.gen_w_concat(w, 0, DEV), cfg, device=DEV)
+    other = K().pack_weights((synth.gen_layer(w, j, 1, DEV, "random") for j in range(2)),
+                             synth.gen_w_concat(w, 1, DEV), cfg, device=DEV)
+    m = K().Kraken(cfg)
+    X = synth.gen_hidden(w, T, 0, DEV)
+    m.load_weights(blob)
+    o1, s1 = m.prefill(X, [0, T], sub_out=True)
+    o1, s1 = o1.clone(), s1.clone()
+    m.load_weights(other)
+    m.load_weights(blob)
+    m.load_weights(blob)
+    o2, s2 = m.prefill(X, [0, T], sub_out=True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(s1, s2)
+    m.close()
+
+
 def test_bf16_operands_n4_l12_d768_prefix():
     # bf16 MFMA operands (no fp16 conversion): within the bound at this depth
     w = dataclasses.replace(synth.workload("kraken-n4-l12-d768-h12-s2048-bf16"), compute="bf16")
