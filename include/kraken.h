@@ -34,6 +34,12 @@
  *     Device work is asynchronous and ordered on that stream.
  *   - Device pointers must be device memory of the device that was current
  *     when the model was created; that device must be current at every call.
+ *   - Debug switch: with the environment variable KRAKEN_DEBUG_SYNC set to a
+ *     value other than "0" when a model is created, every kernel launch of that
+ *     model's prefill / decode calls is followed by a synchronisation of the
+ *     stream; a launch or execution error is then returned (KRAKEN_ERR_HIP,
+ *     naming the kernel) by the call that enqueued it instead of surfacing at a
+ *     later synchronisation.  Results are bit-identical to a normal run.
  */
 #ifndef KRAKEN_H_
 #define KRAKEN_H_
@@ -51,7 +57,8 @@ typedef enum {
   KRAKEN_ERR_UNSUPPORTED = 2,  /* a valid configuration the library does not implement */
   KRAKEN_ERR_OOM = 3,          /* device allocation failed; nothing is leaked */
   KRAKEN_ERR_STATE = 4,        /* e.g. kraken_prefill before kraken_load_weights */
-  KRAKEN_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed */
+  KRAKEN_ERR_HIP = 5,          /* a HIP runtime call or kernel launch failed */
+  KRAKEN_ERR_OVERFLOW = 6      /* kraken_sync: an activation exceeded the fp16 operand range */
 } kraken_status;
 
 typedef enum {
@@ -79,7 +86,9 @@ typedef enum {
  *   n_layers   L >= 1
  *   d_model    d, width of one sub-layer; multiple of 64
  *   n_heads    heads per sub-layer; d / n_heads must be 32, 64 or 128
- *   d_ff       MLP width; 0 means 4 d (Section 2.1); multiple of 64
+ *   d_ff       MLP width; 0 means 4 d (Section 2.1); multiple of 64;
+ *              d_ff * d * 4 < 2^31 and n_sub * d^2 * 4 < 2^31 (the repacked FFN and
+ *              W_concat weights are addressed with 32-bit byte offsets)
  *   max_tokens largest packed token count T a prefill may use (>= 1; at most
  *              4194304, and max_tokens * max(2 d, d_ff) * 4 < 2^31)
  *   dtype      a kraken_dtype: element type of the weight blob and of hidden_in
@@ -121,7 +130,7 @@ typedef struct kraken_model kraken_model;
  * The model owns that memory until kraken_destroy.  *out is set to NULL on
  * failure.  Errors: INVALID_ARG (null pointers, non-positive sizes),
  * UNSUPPORTED (d or d_ff not a multiple of 64, head size not 32/64/128,
- * unknown dtype), OOM.
+ * unknown dtype, sizes past the 32-bit offset limits above), OOM.
  */
 kraken_status kraken_create(const kraken_config* cfg, kraken_model** out);
 
@@ -232,6 +241,21 @@ kraken_status kraken_decode(kraken_model* m, const void* hidden_in, const int32_
                             int32_t num_seqs, float* hidden_out, float* sub_out, void* kv_cache,
                             int32_t max_seqs, int32_t capacity, void* stream);
 
+/*
+ * Waits for `stream` and reports the model's fp16 activation overflow flag.
+ * With fp16 MFMA operands (compute type KRAKEN_COMPUTE_F16, or fp16 storage),
+ * every activation converted to fp16 for a matrix product (the LayerNorm
+ * outputs, the Q|K and V projections, the GELU output and the high half of
+ * the W_concat operand) is checked on the device: a finite fp32 value of
+ * magnitude >= 65520 rounds to an fp16 infinity and sets a sticky flag.  (The
+ * attention output is a convex combination of V rows and cannot exceed the
+ * V projection's range.)  Returns KRAKEN_ERR_OVERFLOW, and clears the flag, if
+ * any kraken_prefill / kraken_prefill_kv / kraken_decode of this model since
+ * the last kraken_sync overflowed: their outputs are then not valid.  Returns
+ * KRAKEN_OK otherwise.  Errors: INVALID_ARG, HIP.
+ */
+kraken_status kraken_sync(kraken_model* m, void* stream);
+
 /* Waits for the model's device work, frees everything it owns.  NULL is a no-op. */
 kraken_status kraken_destroy(kraken_model* m);
 
@@ -311,6 +335,14 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
                              int64_t sR, void* stream);
 
 /*
+ * Test support: fills the model's whole activation workspace with 0xFF bytes
+ * (a NaN in every element type) on `stream`.  A following prefill or decode
+ * must give the same result as without it: every workspace element a kernel
+ * reads has been written earlier in the same call.  Errors: INVALID_ARG, HIP.
+ */
+kraken_status kraken_debug_poison_workspace(kraken_model* m, void* stream);
+
+/*
  * kraken_op_attention (Section 2.1, causal MHA core; packed sequences), with
  * n_kv_heads key/value heads (0 = n_heads; query head h reads key/value head
  * h / (n_heads / n_kv_heads)) and dkv = n_kv_heads * hd:
@@ -320,11 +352,17 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
  *      ldv = T rounded up to a multiple of 64 (KRAKEN_VT_LD(T)); the padding
  *      columns [T, ldv) must hold finite values (they meet zero probabilities),
  *   out S [n][T][d]: out = softmax(Q K^T / sqrt(hd) + causal mask) V per head.
+ *   q_prescaled 0: Q as above.  1: the Q columns already carry the factor
+ *      log2(e) / sqrt(hd), as kraken_prefill's Q projection does (its weights are
+ *      scaled at load), and the kernel computes softmax with base-2 exponentials
+ *      of Q K^T directly: out = softmax(ln(2) Q K^T + mask) V.  This is the
+ *      variant the prefill launches.
  *   cu_seqlens is a HOST int32[num_seqs+1] array as in kraken_prefill.
  */
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
                                   int32_t n, int32_t d, int32_t n_heads, int32_t n_kv_heads,
-                                  const int32_t* cu_seqlens, int32_t num_seqs, void* stream);
+                                  int32_t q_prescaled, const int32_t* cu_seqlens,
+                                  int32_t num_seqs, void* stream);
 
 /*
  * kraken_op_decode_attention (Section 2.1, attention of one new token per

@@ -45,6 +45,7 @@ struct GemmParams {
   int64_t gA, gB;
   int gBmod;
   int tiles_m, tiles_n, batch;
+  int* ovf;                // fp16 outputs: overflow flag (NULL: not checked)
 };
 
 // GELU(v) = v Phi(v) with Phi the standard normal CDF.  With h = Phi(-|v|) this is
@@ -71,6 +72,22 @@ __device__ __forceinline__ float gelu_erf(float v) {
 template <typename S>
 __device__ __forceinline__ void store_val(S* p, float v) {
   *p = static_cast<S>(v);
+}
+
+// fp16 overflow check of the epilogues: a value of magnitude >= 65520 rounds (to nearest
+// even) to an fp16 infinity.  amax tracks the largest magnitude a thread stores; at the end
+// one lane of each wave that saw an overflow sets the flag with a vector store.
+constexpr float F16_OVERFLOW = 65520.0f;
+template <typename OutT>
+__device__ __forceinline__ void track4(float& amax, float4 v) {
+  if constexpr (__is_same(OutT, f16))
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+}
+template <typename OutT>
+__device__ __forceinline__ void flag_overflow(float amax, int* ovf) {
+  if constexpr (__is_same(OutT, f16)) {
+    if (ovf && __ballot(!(amax < F16_OVERFLOW)) && (threadIdx.x & 63) == 0) *ovf = 1;
+  }
 }
 
 // Four consecutive outputs of a row segment, stored non-temporally: a tile's outputs are
@@ -399,6 +416,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
   const float* Rz = p.R ? p.R + z * p.sR : nullptr;
   OutT* Cz = static_cast<OutT*>(p.C) + z * p.sC;
   const bool vec_ok = (p.ldc & 3) == 0;
+  float amax = 0.f;                                    // fp16 outputs: largest |value|
   // the whole tile inside C, with 16-byte-aligned row segments (uniform per workgroup)
   const bool interior = vec_ok && m0 + BM <= p.M && n0 + BN <= p.N;
   const int rows0 = m0 + wm * TM, cols0 = n0 + wn * TN;
@@ -468,6 +486,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
             v.x += rr.x; v.y += rr.y; v.z += rr.z; v.w += rr.w;
           }
           const int m = rows0 + i * 32 + seg_ml(q), n = cols0 + seg_nl(q);
+          track4<OutT>(amax, v);
           store4<OutT>(Cz + (int64_t)m * p.ldc + n, v);
         }
       }
@@ -492,6 +511,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
           const float4 rr = rbuf[q / QH][q % QH];
           v.x += rr.x; v.y += rr.y; v.z += rr.z; v.w += rr.w;
         }
+        track4<OutT>(amax, v);
         store4<OutT>(dst, v);
       } else {
         const float vv[4] = {v.x, v.y, v.z, v.w};
@@ -502,6 +522,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
           if constexpr (EPI == EPI_BIAS_N_RES) {
             if (Rz) o += Rz[(int64_t)m * p.ldc + n + k];
           }
+          track4<OutT>(amax, make_float4(o, 0.f, 0.f, 0.f));
           store_val<OutT>(dst + k, o);
         }
       }
@@ -513,6 +534,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmParams p) {
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
   }
+  flag_overflow<OutT>(amax, p.ovf);
 }
 
 template <typename S, int BM, int BN>
@@ -526,6 +548,7 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t s) {
   p.tiles_m = (g.M + BM - 1) / BM;
   p.tiles_n = (g.N + BN - 1) / BN;
   p.batch = g.batch;
+  p.ovf = g.ovf;
   const int64_t total = (int64_t)p.tiles_m * p.tiles_n * p.batch;
   dim3 grid((unsigned)total), block(256);
   switch (g.epi) {
@@ -672,6 +695,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmParams p) {
   __syncthreads();
   const int tid = threadIdx.x;
   const float* biasz = p.bias ? p.bias + z * p.sBias : nullptr;
+  float amax = 0.f;
 #pragma unroll
   for (int w = 0; w < TW; ++w) {
     const int n = n0 + w * 16 + (tid & 15);
@@ -687,9 +711,11 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmParams p) {
       if constexpr (EPI == EPI_BIAS_N_RES) {
         if (p.R) v += p.R[z * p.sR + (int64_t)m * p.ldc + n];
       }
+      track4<OutT>(amax, make_float4(v, 0.f, 0.f, 0.f));
       store_val<OutT>(static_cast<OutT*>(p.C) + z * p.sC + (int64_t)m * p.ldc + n, v);
     }
   }
+  flag_overflow<OutT>(amax, p.ovf);
 }
 
 template <typename S, int MB, int TW>
@@ -701,6 +727,7 @@ hipError_t launch_skinny(const GemmDesc& g, hipStream_t s) {
   p.sA = g.sA; p.sB = g.sB; p.sC = g.sC; p.sR = g.sR; p.sBias = g.sBias;
   p.kgroups = g.kgroups; p.gA = g.gA; p.gB = g.gB; p.gBmod = g.gBmod;
   p.tiles_m = 1; p.tiles_n = (g.N + 16 * TW - 1) / (16 * TW); p.batch = g.batch;
+  p.ovf = g.ovf;
   dim3 grid((unsigned)p.tiles_n, (unsigned)g.batch), block(256);
   switch (g.epi) {
     case EPI_BIAS_N:

@@ -74,6 +74,9 @@ struct GemmDesc {
   int kgroups;
   int64_t gA, gB;
   int gBmod;
+  // fp16 outputs only: set to 1 (vector store) when a finite fp32 result rounds to an
+  // fp16 infinity (|v| >= 65520); NULL: no check
+  int* ovf;
 };
 
 hipError_t launch_gemm(const GemmDesc& g, hipStream_t s);
@@ -102,21 +105,23 @@ hipError_t launch_zero_cols(DType dt, void* base, int64_t rows, int64_t ld, int 
                             hipStream_t s);
 
 // LayerNorm of n rows-sets: out[i][t] = LN(x[i*xs + t*d]) with per-i gamma/beta.
+// ovf (fp16 outputs; may be NULL): set to 1 when an output overflows the fp16 range.
 hipError_t launch_layernorm(DType dt, const float* x, int64_t x_batch_stride, const float* gamma,
                             const float* beta, void* out, int n, int T, int d, float eps,
-                            hipStream_t s);
+                            int* ovf, hipStream_t s);
 
-// out[i][t] = LN(h[i][t] + y[t]); y = shared[t] or sum_k x[k][t].
+// out[i][t] = LN(h[i][t] + y[t]); y = shared[t] or sum_k x[k][t].  ovf as for LN1.
 hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
                               const float* gamma, const float* beta, void* out, int n, int T,
-                              int d, float eps, hipStream_t s);
+                              int d, float eps, int* ovf, hipStream_t s);
 
 // dst[k] = float(src[k]) for k < count.
 hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, hipStream_t s);
 
 // Two-term split of fp32 values in a 16-bit type: hi = S(v), lo = S(v - hi);
-// hi at dst, lo at dst + count (elements).
-hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, hipStream_t s);
+// hi at dst, lo at dst + count (elements).  ovf as for LN1 (a hi part that overflows fp16).
+hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, int* ovf,
+                          hipStream_t s);
 
 // dst[c][r] = Dst(src[r*src_ld + c]) for r < R, c < C, dst row stride dst_ld.  When the
 // destination is fp16 and a finite source value does not fit, *overflow is set to 1.

@@ -60,19 +60,37 @@ __device__ __forceinline__ void store4<f16>(f16* dst, float a, float b, float c,
   *reinterpret_cast<f16x4*>(dst) = v;
 }
 
+// Largest magnitude that rounds to a finite fp16 value: |v| >= 65520 rounds (to nearest
+// even) to infinity.
+constexpr float F16_OVERFLOW = 65520.0f;
+
 // Normalise v (this thread's float4s of one row, at most V) and write the row to dst.
+// Returns the largest output magnitude written (for the fp16 overflow check).
 template <typename S, int V>
-__device__ __forceinline__ void ln_write(const float4* v, int nv, float mean, float rstd,
-                                         const float* gamma, const float* beta, S* dst) {
+__device__ __forceinline__ float ln_write(const float4* v, int nv, float mean, float rstd,
+                                          const float* gamma, const float* beta, S* dst) {
   const int tid = threadIdx.x;
+  float amax = 0.f;
 #pragma unroll
   for (int u = 0; u < V; ++u) {
     if (u >= nv) break;
     const int c = (tid + u * NORM_THREADS) * 4;
     const float4 g = *reinterpret_cast<const float4*>(gamma + c);
     const float4 b = *reinterpret_cast<const float4*>(beta + c);
-    store4(dst + c, (v[u].x - mean) * rstd * g.x + b.x, (v[u].y - mean) * rstd * g.y + b.y,
-           (v[u].z - mean) * rstd * g.z + b.z, (v[u].w - mean) * rstd * g.w + b.w);
+    const float o0 = (v[u].x - mean) * rstd * g.x + b.x, o1 = (v[u].y - mean) * rstd * g.y + b.y;
+    const float o2 = (v[u].z - mean) * rstd * g.z + b.z, o3 = (v[u].w - mean) * rstd * g.w + b.w;
+    if constexpr (__is_same(S, f16))
+      amax = fmaxf(amax, fmaxf(fmaxf(fabsf(o0), fabsf(o1)), fmaxf(fabsf(o2), fabsf(o3))));
+    store4(dst + c, o0, o1, o2, o3);
+  }
+  return amax;
+}
+
+// fp16 outputs: one lane of each wave whose outputs overflowed sets *ovf (a vector store).
+template <typename S>
+__device__ __forceinline__ void flag_overflow(float amax, int* ovf) {
+  if constexpr (__is_same(S, f16)) {
+    if (ovf && __ballot(!(amax < F16_OVERFLOW)) && (threadIdx.x & 63) == 0) *ovf = 1;
   }
 }
 
@@ -113,10 +131,12 @@ __device__ __forceinline__ int my_vecs(int d) {
 template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
     const float* __restrict__ x, int64_t xs, const float* __restrict__ gamma,
-    const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, float eps) {
+    const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, float eps,
+    int* __restrict__ ovf) {
   __shared__ float red[NORM_THREADS / 64];
   const int t = blockIdx.x;
   const int nv = my_vecs(d);
+  float amax = 0.f;
   // sub-layers [i0, i1) of this block (gridDim.y blocks share the n sub-layers)
   const int i0 = (int)((int64_t)n * blockIdx.y / gridDim.y);
   const int i1 = (int)((int64_t)n * (blockIdx.y + 1) / gridDim.y);
@@ -130,17 +150,19 @@ __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
         if (u < nv) v[u] = *reinterpret_cast<const float4*>(row + (threadIdx.x + u * NORM_THREADS) * 4);
       row_stats<V>(v, nv, d, eps, red, mean, rstd);
     }
-    ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
-             out + ((int64_t)i * T + t) * d);
+    amax = fmaxf(amax, ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d,
+                                      beta + (int64_t)i * d, out + ((int64_t)i * T + t) * d));
   }
+  flag_overflow<S>(amax, ovf);
 }
 
 template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
     const float* __restrict__ x, const float* __restrict__ shared, const float* __restrict__ h,
     const float* __restrict__ gamma, const float* __restrict__ beta, S* __restrict__ out, int n,
-    int T, int d, float eps) {
+    int T, int d, float eps, int* __restrict__ ovf) {
   __shared__ float red[NORM_THREADS / 64];
+  float amax = 0.f;
   const int t = blockIdx.x;
   const int nv = my_vecs(d);
   const int64_t plane = (int64_t)T * d;
@@ -174,9 +196,10 @@ __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
     }
     float mean, rstd;
     row_stats<V>(v, nv, d, eps, red, mean, rstd);
-    ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d, beta + (int64_t)i * d,
-                   out + (i * plane + (int64_t)t * d));
+    amax = fmaxf(amax, ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d,
+                                      beta + (int64_t)i * d, out + (i * plane + (int64_t)t * d)));
   }
+  flag_overflow<S>(amax, ovf);
 }
 
 template <typename S>
@@ -194,14 +217,18 @@ __global__ void scale_kernel(S* __restrict__ p, int64_t count, float c) {
 }
 
 template <typename S>
-__global__ void split16_kernel(const float* __restrict__ src, S* __restrict__ dst, int64_t count) {
+__global__ void split16_kernel(const float* __restrict__ src, S* __restrict__ dst, int64_t count,
+                               int* __restrict__ ovf) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  float amax = 0.f;
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < count; k += stride) {
     const float v = src[k];
     const S hi = (S)v;
     dst[k] = hi;
     dst[k + count] = (S)(v - (float)hi);
+    amax = fmaxf(amax, fabsf(v));
   }
+  flag_overflow<S>(amax, ovf);
 }
 
 template <typename Src, typename Dst>
@@ -266,7 +293,7 @@ unsigned sub_groups(int n, int T) {
 
 hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* gamma,
                             const float* beta, void* out, int n, int T, int d, float eps,
-                            hipStream_t s) {
+                            int* ovf, hipStream_t s) {
   if (T <= 0 || n <= 0) return hipSuccess;
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
@@ -276,10 +303,10 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
     const dim3 grid(T, xs != 0 ? (unsigned)n : sub_groups(n, T)), block(NORM_THREADS);
     S* o = static_cast<S*>(out);
     switch (vecs_for(d)) {
-      case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
-      case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
-      case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
-      default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps); break;
+      case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
+      default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
     }
     return hipGetLastError();
   });
@@ -287,7 +314,7 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
 
 hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
                               const float* gamma, const float* beta, void* out, int n, int T,
-                              int d, float eps, hipStream_t s) {
+                              int d, float eps, int* ovf, hipStream_t s) {
   if (T <= 0 || n <= 0) return hipSuccess;
   if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
@@ -295,10 +322,10 @@ hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, con
     const dim3 grid(T, sub_groups(n, T)), block(NORM_THREADS);
     S* o = static_cast<S*>(out);
     switch (vecs_for(d)) {
-      case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
-      case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
-      case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
-      default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps); break;
+      case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
+      default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
     }
     return hipGetLastError();
   });
@@ -336,14 +363,15 @@ hipError_t launch_zero_cols(DType dt, void* base, int64_t rows, int64_t ld, int 
   });
 }
 
-hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, hipStream_t s) {
+hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, int* ovf,
+                          hipStream_t s) {
   if (count <= 0) return hipSuccess;
   if (dt == DType::BF16)
     hipLaunchKernelGGL(split16_kernel<bf16>, dim3(grid_for(count)), dim3(256), 0, s, src,
-                       static_cast<bf16*>(dst), count);
+                       static_cast<bf16*>(dst), count, ovf);
   else if (dt == DType::F16)
     hipLaunchKernelGGL(split16_kernel<f16>, dim3(grid_for(count)), dim3(256), 0, s, src,
-                       static_cast<f16*>(dst), count);
+                       static_cast<f16*>(dst), count, ovf);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -13,6 +13,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -95,11 +96,15 @@ struct kraken_model {
   void* amem = nullptr;
   std::vector<LayerW> layers;
   void* WcatT = nullptr;  // [d][N*d]
-  int* flags = nullptr;   // device: [0] = a weight overflowed the operand type
+  // device: [0] = a weight overflowed the operand type (set at load); [1] = an activation
+  // overflowed the fp16 operand type (sticky until kraken_sync reads it)
+  int* flags = nullptr;
   // workspace
   float *X32 = nullptr, *xbuf = nullptr, *hbuf = nullptr;
   void *act = nullptr, *qk = nullptr, *vt = nullptr, *o = nullptr, *g = nullptr;
   char* ws_end = nullptr;
+  // KRAKEN_DEBUG_SYNC=1 at kraken_create: synchronise and check after every launch
+  bool debug_sync = false;
   // per-kernel timing
   bool prof = false;
   std::vector<ProfRec> pending;
@@ -118,16 +123,26 @@ struct kraken_model {
     return e;
   }
 
-  // Runs one launch, bracketed by timing events when profiling is on.
+  // Runs one launch, bracketed by timing events when profiling is on; in debug-sync mode
+  // the stream is synchronised after it and any launch or execution error is returned.
   template <class Fn>
   hipError_t run(int cls, hipStream_t s, Fn&& fn) {
-    if (!prof) return fn();
-    hipEvent_t a = take_event(), b = take_event();
-    if (!a || !b) return fn();
-    hipEventRecord(a, s);
-    hipError_t e = fn();
-    hipEventRecord(b, s);
-    pending.push_back({cls, a, b});
+    hipError_t e;
+    hipEvent_t a = prof ? take_event() : nullptr, b = prof ? take_event() : nullptr;
+    if (a && b) {
+      hipEventRecord(a, s);
+      e = fn();
+      hipEventRecord(b, s);
+      pending.push_back({cls, a, b});
+    } else {
+      if (a) pool.push_back(a);
+      if (b) pool.push_back(b);
+      e = fn();
+    }
+    if (e == hipSuccess && debug_sync) {
+      e = hipStreamSynchronize(s);
+      if (e == hipSuccess) e = hipGetLastError();
+    }
     return e;
   }
 };
@@ -158,9 +173,16 @@ kraken_status validate_cfg(const kraken_config* c) {
   }
   if (c->d_model > 8192) return fail(KRAKEN_ERR_UNSUPPORTED, "d_model above 8192");
   if (c->max_tokens > (1 << 22)) return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens above 4194304");
-  // GEMM operands of one sub-layer are addressed with 32-bit byte offsets
+  // GEMM operands of one sub-layer are addressed with 32-bit byte offsets: the activation
+  // rows (tokens x the widest row), and the repacked weights [out][in] of the FFN (F x d
+  // either way) and of W_concat (d x N d); 4 bytes bounds every element type
   if ((int64_t)c->max_tokens * std::max(2 * c->d_model, F) * 4 >= (1ll << 31))
     return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens * max(2 d_model, d_ff) too large");
+  if ((int64_t)F * c->d_model * 4 >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "d_ff * d_model too large for 32-bit weight offsets");
+  if ((int64_t)c->n_sub * c->d_model * c->d_model * 4 >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED,
+                "n_sub * d_model^2 too large for 32-bit W_concat offsets");
   if (c->dtype < KRAKEN_DTYPE_F32 || c->dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
   if (c->compute < KRAKEN_COMPUTE_STORAGE || c->compute > KRAKEN_COMPUTE_F16)
@@ -340,6 +362,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
                       hipStream_t s) {
   const bool decode = kv && kv->lens;
   const DType dt = m->dt;
+  int* const ovf = m->flags + 1;   // fp16 operand overflow of the activations
   const int64_t N = m->N, d = m->d, F = m->F;
   const int64_t Td = (int64_t)T * d;
   const int ldv = vt_ld(T);
@@ -368,7 +391,8 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
     const int64_t xs = j == 0 ? 0 : Td;           // first layer: one shared input
     char* cache_j = kv ? kv->cache + (size_t)j * kv->layer_bytes : nullptr;
     RUN(KRAKEN_K_LN1,
-        launch_layernorm(dt, xin, xs, w.ln1_g, w.ln1_b, m->act, (int)N, T, (int)d, m->eps, s),
+        launch_layernorm(dt, xin, xs, w.ln1_g, w.ln1_b, m->act, (int)N, T, (int)d, m->eps, ovf,
+                         s),
         "ln1");
     {
       GemmDesc g = gemm_base(dt);
@@ -378,6 +402,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
       g.C = m->qk; g.ldc = (int)dqk; g.sC = (int64_t)T * dqk;
       g.bias = w.bqk; g.sBias = dqk;
       g.M = T; g.N = (int)dqk; g.K = (int)d; g.batch = (int)N;
+      g.ovf = ovf;
       RUN(KRAKEN_K_GEMM_QK, launch_gemm(g, s), "QK projection");
     }
     if (!decode) {
@@ -389,6 +414,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
         g.C = m->vt; g.ldc = ldv; g.sC = dkv * ldv;
         g.bias = w.bv; g.sBias = dkv;
         g.M = (int)dkv; g.N = T; g.K = (int)d; g.batch = (int)N;
+        g.ovf = ovf;
         RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
       }
       if (kv)
@@ -413,6 +439,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
         g.C = m->o; g.ldc = (int)dkv; g.sC = (int64_t)T * dkv;
         g.bias = w.bv; g.sBias = dkv;
         g.M = T; g.N = (int)dkv; g.K = (int)d; g.batch = (int)N;
+        g.ovf = ovf;
         RUN(KRAKEN_K_GEMM_VT, launch_gemm(g, s), "V projection");
       }
       RUN(KRAKEN_K_KV,
@@ -438,7 +465,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
     }
     RUN(KRAKEN_K_COMBINE,
         launch_combine_ln2(dt, m->xbuf, j == 0 ? X32 : nullptr, m->hbuf, w.ln2_g, w.ln2_b, m->act,
-                           (int)N, T, (int)d, m->eps, s),
+                           (int)N, T, (int)d, m->eps, ovf, s),
         "combine + ln2");
     {
       GemmDesc g = gemm_base(dt);
@@ -448,6 +475,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
       g.C = m->g; g.ldc = (int)F; g.sC = (int64_t)T * F;
       g.bias = w.b1; g.sBias = F;
       g.M = T; g.N = (int)F; g.K = (int)d; g.batch = (int)N;
+      g.ovf = ovf;
       RUN(KRAKEN_K_GEMM_UP, launch_gemm(g, s), "FFN up");
     }
     {
@@ -474,7 +502,7 @@ kraken_status forward(kraken_model* m, const void* hidden_in, int T, const int32
     g.epi = EPI_BIAS_N_RES;
     if (dt != DType::F32) {
       // 16-bit operands: Y = hi + lo with hi = S(Y), lo = S(Y - hi); 2N groups
-      RUN(KRAKEN_K_CONCAT, launch_split16(dt, m->xbuf, m->g, N * Td, s),
+      RUN(KRAKEN_K_CONCAT, launch_split16(dt, m->xbuf, m->g, N * Td, ovf, s),
           "W_concat operand split");
       g.A = m->g;
       g.kgroups = (int)(2 * N);
@@ -517,6 +545,7 @@ const char* kraken_status_string(kraken_status s) {
     case KRAKEN_ERR_OOM: return "out of device memory";
     case KRAKEN_ERR_STATE: return "invalid state";
     case KRAKEN_ERR_HIP: return "HIP error";
+    case KRAKEN_ERR_OVERFLOW: return "fp16 activation overflow";
   }
   return "unknown status";
 }
@@ -553,6 +582,10 @@ kraken_status kraken_create(const kraken_config* cfg, kraken_model** out) {
   m->F = cfg->d_ff ? cfg->d_ff : 4 * cfg->d_model;
   m->Tmax = cfg->max_tokens;
   m->eps = cfg->ln_eps > 0.f ? cfg->ln_eps : 1e-5f;
+  {
+    const char* dbg = std::getenv("KRAKEN_DEBUG_SYNC");
+    m->debug_sync = dbg && dbg[0] && std::strcmp(dbg, "0") != 0;
+  }
   hipError_t e = hipGetDevice(&m->device);
   if (e != hipSuccess) {
     delete m;
@@ -771,6 +804,35 @@ kraken_status kraken_decode(kraken_model* m, const void* hidden_in, const int32_
                  static_cast<hipStream_t>(stream));
 }
 
+kraken_status kraken_sync(kraken_model* m, void* stream) {
+  if (!m) return fail(KRAKEN_ERR_INVALID_ARG, "model is NULL");
+  kraken_status st = check_device(m);
+  if (st != KRAKEN_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int flag = 0;
+  HIP_TRY(hipMemcpyAsync(&flag, m->flags + 1, sizeof(int), hipMemcpyDeviceToHost, s),
+          "overflow flag read");
+  HIP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+  if (flag) {
+    HIP_TRY(hipMemsetAsync(m->flags + 1, 0, sizeof(int), s), "overflow flag reset");
+    HIP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+    return fail(KRAKEN_ERR_OVERFLOW,
+                "an activation exceeded the fp16 operand range since the last kraken_sync; "
+                "the outputs of those calls are not valid");
+  }
+  return KRAKEN_OK;
+}
+
+kraken_status kraken_debug_poison_workspace(kraken_model* m, void* stream) {
+  if (!m) return fail(KRAKEN_ERR_INVALID_ARG, "model is NULL");
+  kraken_status st = check_device(m);
+  if (st != KRAKEN_OK) return st;
+  const size_t bytes = (size_t)(m->ws_end - static_cast<char*>(m->amem));
+  HIP_TRY(hipMemsetAsync(m->amem, 0xff, bytes, static_cast<hipStream_t>(stream)),
+          "workspace poison");
+  return KRAKEN_OK;
+}
+
 kraken_status kraken_profile_enable(kraken_model* m, int enable) {
   if (!m) return fail(KRAKEN_ERR_INVALID_ARG, "model is NULL");
   m->prof = enable != 0;
@@ -847,7 +909,7 @@ kraken_status kraken_op_layernorm(int32_t dtype, const float* x, int64_t xs, con
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
   if (n < 1 || T < 0 || d < 4 || d % 64 != 0 || d > 8192 || xs < 0)
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
-  hipError_t e = launch_layernorm((DType)dtype, x, xs, gamma, beta, out, n, T, d, eps,
+  hipError_t e = launch_layernorm((DType)dtype, x, xs, gamma, beta, out, n, T, d, eps, nullptr,
                                   static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "layernorm");
 }
@@ -863,7 +925,7 @@ kraken_status kraken_op_combine_ln2(int32_t dtype, const float* x, const float* 
   if (n < 1 || T < 0 || d % 64 != 0 || d < 64 || d > 8192)
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
   hipError_t e = launch_combine_ln2((DType)dtype, x, shared, h, gamma, beta, out, n, T, d, eps,
-                                    static_cast<hipStream_t>(stream));
+                                    nullptr, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "combine_ln2");
 }
 
@@ -890,7 +952,8 @@ kraken_status kraken_op_gemm(int32_t dtype, int32_t epilogue, const void* A, con
 
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
                                   int32_t n, int32_t d, int32_t n_heads, int32_t n_kv_heads,
-                                  const int32_t* cu_seqlens, int32_t num_seqs, void* stream) {
+                                  int32_t q_prescaled, const int32_t* cu_seqlens,
+                                  int32_t num_seqs, void* stream) {
   if (!qk || !vt || !out) return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
   if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
@@ -907,7 +970,7 @@ kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt,
   a.dt = (DType)dtype; a.qk = qk; a.vt = vt; a.out = out;
   a.n = n; a.T = (int)T; a.d = d; a.n_heads = n_heads; a.n_kv_heads = n_kv_heads;
   a.cu_host = cu_seqlens; a.num_seqs = num_seqs;
-  a.q_prescaled = 0;
+  a.q_prescaled = q_prescaled != 0;
   hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "attention");
 }

@@ -18,7 +18,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkraken.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OOM, ERR_STATE, ERR_HIP = range(6)
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OOM, ERR_STATE, ERR_HIP, ERR_OVERFLOW = range(7)
 DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 COMPUTE_CODES = {"storage": 0, "f32": 1, "bf16": 2, "f16": 3}
 MAX_SEQS = 256
@@ -75,6 +75,8 @@ def lib() -> ctypes.CDLL:
         "kraken_prefill_kv": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
         "kraken_decode": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
         "kraken_destroy": ([vp], i32),
+        "kraken_sync": ([vp, vp], i32),
+        "kraken_debug_poison_workspace": ([vp, vp], i32),
         "kraken_status_string": ([i32], ctypes.c_char_p),
         "kraken_last_error": ([], ctypes.c_char_p),
         "kraken_profile_enable": ([vp, ctypes.c_int], i32),
@@ -85,7 +87,8 @@ def lib() -> ctypes.CDLL:
         "kraken_op_combine_ln2": ([i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, fp, vp], i32),
         "kraken_op_gemm": ([i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, i64, i64, i64,
                             vp], i32),
-        "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32), i32, vp], i32),
+        "kraken_op_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, i32, P(i32), i32, vp],
+                                i32),
         "kraken_op_decode_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32), i32, i32,
                                         i32, vp, i64, vp], i32),
     }
@@ -115,6 +118,34 @@ def _stream(stream) -> Optional[int]:
 def _cu_array(cu: Sequence[int]):
     arr = (ctypes.c_int32 * len(cu))(*[int(v) for v in cu])
     return arr
+
+
+def check_device_tensor(name: str, t: torch.Tensor, dtype: torch.dtype, numel: int,
+                        device: Optional[torch.device] = None) -> None:
+    """Raises ValueError unless ``t`` is a contiguous GPU tensor of ``dtype`` with exactly
+    ``numel`` elements (on ``device`` when given): what the C ABI's device pointers need."""
+    if not getattr(t, "is_cuda", False):
+        raise ValueError(f"{name} must be a GPU tensor (got {getattr(t, 'device', type(t))})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+
+
+def check_call_buffers(cfg: "Config", hidden: torch.Tensor, rows: int,
+                       out: Optional[torch.Tensor], sub_out: Optional[torch.Tensor]) -> None:
+    """Validates the buffers of a prefill / decode call of ``rows`` token rows."""
+    d = cfg.d_model
+    check_device_tensor("hidden", hidden, torch_dtype(dtype_code(cfg.dtype)), rows * d)
+    if out is not None:
+        check_device_tensor("out", out, torch.float32, rows * d, hidden.device)
+    if sub_out is not None:
+        check_device_tensor("sub_out", sub_out, torch.float32, cfg.n_sub * rows * d,
+                            hidden.device)
 
 
 def cu_from_lens(seq_lens: Sequence[int]) -> List[int]:
@@ -256,14 +287,7 @@ class Kraken:
                 stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
         """Runs the prefill; returns (out [T, d] fp32, sub_out [N, T, d] fp32 or None)."""
         T = int(cu_seqlens[-1])
-        d = self.cfg.d_model
-        if out is None:
-            out = torch.empty((T, d), dtype=torch.float32, device=hidden.device)
-        if sub_out is True:
-            sub_out = torch.empty((self.cfg.n_sub, T, d), dtype=torch.float32,
-                                  device=hidden.device)
-        elif sub_out is False:
-            sub_out = None
+        out, sub_out = self._outputs(hidden, T, out, sub_out)
         cu = _cu_array(cu_seqlens)
         _check(lib().kraken_prefill(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
                                     out.data_ptr(), _ptr(sub_out), _stream(stream)))
@@ -287,6 +311,7 @@ class Kraken:
         """prefill() that also writes sequence b's keys and values into slot b of cache."""
         T = int(cu_seqlens[-1])
         out, sub_out = self._outputs(hidden, T, out, sub_out)
+        self._check_cache(cache, hidden)
         cu = _cu_array(cu_seqlens)
         _check(lib().kraken_prefill_kv(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
                                        out.data_ptr(), _ptr(sub_out), cache.buf.data_ptr(),
@@ -301,6 +326,7 @@ class Kraken:
         fp32; the caller advances lens by one."""
         B = len(lens)
         out, sub_out = self._outputs(hidden, B, out, sub_out)
+        self._check_cache(cache, hidden)
         arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
         _check(lib().kraken_decode(self._h, hidden.data_ptr(), arr, B, out.data_ptr(),
                                    _ptr(sub_out), cache.buf.data_ptr(), cache.max_seqs,
@@ -308,6 +334,9 @@ class Kraken:
         return out, sub_out
 
     def _outputs(self, hidden, T, out, sub_out):
+        """Allocates the outputs that are not given and validates every buffer (a contiguous
+        GPU tensor of the right dtype and size), so that no host pointer, short buffer or
+        wrong element type reaches the kernels."""
         d = self.cfg.d_model
         if out is None:
             out = torch.empty((T, d), dtype=torch.float32, device=hidden.device)
@@ -316,7 +345,29 @@ class Kraken:
                                   device=hidden.device)
         elif sub_out is False:
             sub_out = None
+        check_call_buffers(self.cfg, hidden, T, out, sub_out)
         return out, sub_out
+
+    def _check_cache(self, cache: "KVCache", hidden: torch.Tensor) -> None:
+        need = self.kv_cache_bytes(cache.max_seqs, cache.capacity)
+        if need == 0:
+            raise ValueError("invalid cache max_seqs or capacity")
+        buf = cache.buf
+        if not buf.is_cuda or buf.device != hidden.device or not buf.is_contiguous():
+            raise ValueError("the cache must be a contiguous GPU tensor on the input's device")
+        if buf.numel() * buf.element_size() < need:
+            raise ValueError(f"the cache holds {buf.numel() * buf.element_size()} bytes, "
+                             f"{need} needed")
+
+    # ---- overflow check and test support
+    def sync(self, stream=None) -> None:
+        """Waits for the stream; raises KrakenError(ERR_OVERFLOW) if an activation exceeded
+        the fp16 operand range in a call since the last sync (kraken_sync)."""
+        _check(lib().kraken_sync(self._h, _stream(stream)))
+
+    def poison_workspace(self, stream=None) -> None:
+        """Fills the model's activation workspace with NaN bytes (test support)."""
+        _check(lib().kraken_debug_poison_workspace(self._h, _stream(stream)))
 
     # ---- per-kernel timing
     def profile_enable(self, on: bool = True) -> None:
@@ -369,11 +420,14 @@ def vt_ld(T: int) -> int:
 
 def op_attention(qk: torch.Tensor, vt: torch.Tensor, out: torch.Tensor, n: int, d: int,
                  n_heads: int, cu_seqlens: Sequence[int], stream=None,
-                 n_kv_heads: int = 0) -> torch.Tensor:
+                 n_kv_heads: int = 0, q_prescaled: bool = False) -> torch.Tensor:
+    """Causal attention of packed sequences.  q_prescaled: the Q columns already carry
+    log2(e) / sqrt(hd) (the form the prefill's Q projection produces)."""
     cu = _cu_array(cu_seqlens)
     _check(lib().kraken_op_attention(dtype_code(qk.dtype), qk.data_ptr(), vt.data_ptr(),
-                                     out.data_ptr(), n, d, n_heads, n_kv_heads, cu,
-                                     len(cu_seqlens) - 1, _stream(stream)))
+                                     out.data_ptr(), n, d, n_heads, n_kv_heads,
+                                     1 if q_prescaled else 0, cu, len(cu_seqlens) - 1,
+                                     _stream(stream)))
     return out
 
 

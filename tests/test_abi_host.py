@@ -150,3 +150,86 @@ def test_grouped_query_sizes():
 ])
 def test_create_rejects_bad_kv_heads(kw, status):
     assert _create_status(**kw) == status
+
+
+@pytest.mark.parametrize("kw", [
+    # repacked FFN weights F x d past 2^31 bytes at 4 bytes an element
+    dict(d_model=8192, n_heads=64, d_ff=65536, max_tokens=1),
+    # W_concat^T d x N d past 2^31 bytes
+    dict(n_sub=16, d_model=8192, n_heads=64, d_ff=8192, max_tokens=1),
+])
+def test_create_rejects_weight_offsets_past_32_bits(kw):
+    assert _create_status(**kw) == K().ERR_UNSUPPORTED
+    assert b"32-bit" in K().lib().kraken_last_error()
+
+
+def test_sync_and_poison_reject_null_model():
+    L = K().lib()
+    assert L.kraken_sync(None, None) == K().ERR_INVALID_ARG
+    assert L.kraken_debug_poison_workspace(None, None) == K().ERR_INVALID_ARG
+    assert L.kraken_status_string(K().ERR_OVERFLOW) == b"fp16 activation overflow"
+
+
+def test_op_attention_validates_before_launch():
+    # a head size the kernels do not have, and a bad cu_seqlens: rejected on the host
+    L = K().lib()
+    cu = (ctypes.c_int32 * 2)(0, 4)
+    dummy = ctypes.c_void_p(16)
+    assert L.kraken_op_attention(2, dummy, dummy, dummy, 1, 96, 1, 0, 1, cu, 1,
+                                 None) == K().ERR_UNSUPPORTED
+    bad = (ctypes.c_int32 * 3)(0, 4, 4)
+    assert L.kraken_op_attention(2, dummy, dummy, dummy, 1, 256, 2, 0, 1, bad, 2,
+                                 None) == K().ERR_INVALID_ARG
+
+
+# ------------------------------------------- the binding's buffer checks (no GPU needed)
+
+def _cfg():
+    return K().Config(n_sub=2, n_layers=1, d_model=128, n_heads=4, max_tokens=16, dtype="bf16")
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    x = torch.zeros((8, 128), dtype=torch.bfloat16)          # CPU: would be a host pointer
+    with pytest.raises(ValueError, match="GPU tensor"):
+        K().check_call_buffers(_cfg(), x, 8, None, None)
+
+
+class _FakeCuda:
+    """Stands in for a CUDA tensor on a host without a GPU: the attributes the binding's
+    buffer checks read, taken from a CPU tensor."""
+
+    def __init__(self, t, index=0):
+        self._t = t
+        self.is_cuda = True
+        self.device = __import__("torch").device("cuda", index)
+        self.dtype = t.dtype
+
+    def is_contiguous(self):
+        return self._t.is_contiguous()
+
+    def numel(self):
+        return self._t.numel()
+
+
+def test_binding_rejects_wrong_dtype_size_layout_and_device():
+    import torch
+    cfg = _cfg()
+    ok = _FakeCuda(torch.zeros((8, 128), dtype=torch.bfloat16))
+    out_ok = _FakeCuda(torch.zeros((8, 128), dtype=torch.float32))
+    sub_ok = _FakeCuda(torch.zeros((2, 8, 128), dtype=torch.float32))
+    K().check_call_buffers(cfg, ok, 8, out_ok, sub_ok)            # accepted
+    cases = [
+        (dict(hidden=_FakeCuda(torch.zeros((8, 128), dtype=torch.float32))), "dtype"),
+        (dict(hidden=_FakeCuda(torch.zeros((7, 128), dtype=torch.bfloat16))), "elements"),
+        (dict(hidden=_FakeCuda(torch.zeros((128, 8), dtype=torch.bfloat16).t())), "contiguous"),
+        (dict(out=_FakeCuda(torch.zeros((8, 128), dtype=torch.bfloat16))), "dtype"),
+        (dict(out=_FakeCuda(torch.zeros((8, 128), dtype=torch.float32), index=1)), "is on"),
+        (dict(out=torch.zeros((8, 128), dtype=torch.float32)), "GPU tensor"),
+        (dict(sub_out=_FakeCuda(torch.zeros((1, 8, 128), dtype=torch.float32))), "elements"),
+    ]
+    for kw, pat in cases:
+        args = dict(hidden=ok, out=out_ok, sub_out=sub_ok)
+        args.update(kw)
+        with pytest.raises(ValueError, match=pat):
+            K().check_call_buffers(cfg, args["hidden"], 8, args["out"], args["sub_out"])

@@ -72,8 +72,9 @@ def prefill_then_decode(w, lens, steps=2, seed=0, affine="random", capacity=None
     cv = cache.view(model.cfg)
     X = synth.gen_hidden(w, T, seed, DEV)
     out_p, sub_p = model.prefill(X, cu, sub_out=True)
+    model.poison_workspace()           # no stale value of the plain prefill may be read
     out, sub = model.prefill_kv(X, cu, cache, sub_out=True)
-    torch.cuda.synchronize()
+    model.sync()
     assert torch.equal(out, out_p) and torch.equal(sub, sub_p), "prefill_kv != prefill"
 
     layers = [list(l) for l in oracle_layers(w, seed, affine)]
@@ -97,8 +98,9 @@ def prefill_then_decode(w, lens, steps=2, seed=0, affine="random", capacity=None
     cur = list(lens)
     for step in range(steps):
         Xn = synth.gen_hidden(w, B, seed + 1 + step, DEV)
+        model.poison_workspace()
         out_d, sub_d = model.decode(Xn, cur, cache, sub_out=True)
-        torch.cuda.synchronize()
+        model.sync()
         out_do, sub_do, kv_new = O.kraken_decode(f64(Xn), cache_o, layers, wconcat(w, seed),
                                                  w.n_heads, n_kv_heads=w.kv_heads)
         check(f"step {step} out", out_d, out_do, bound)
@@ -255,10 +257,24 @@ def test_decode_and_prefill_kv_argument_errors():
     assert status(lambda: model.decode(X[:3], [0, 0, 0], cache)) == kr.ERR_INVALID_ARG
     # a sequence longer than the capacity; more sequences than slots
     assert status(lambda: model.prefill_kv(X, [0, 5, 8], cache)) == kr.ERR_INVALID_ARG
-    assert status(lambda: model.prefill_kv(X, [0, 2, 4, 6], cache)) == kr.ERR_INVALID_ARG
-    # a misaligned cache
-    bad = kr.KVCache(cache.buf[8:], cache.max_seqs, cache.capacity)
+    assert status(lambda: model.prefill_kv(X[:6], [0, 2, 4, 6], cache)) == kr.ERR_INVALID_ARG
+    # a misaligned cache (large enough, 8 bytes off the 16-byte alignment)
+    roomy = model.new_kv_cache(2, 5)
+    bad = kr.KVCache(roomy.buf[8:], cache.max_seqs, cache.capacity)
     assert status(lambda: model.decode(X[:2], [0, 0], bad)) == kr.ERR_INVALID_ARG
+    # a cache buffer shorter than its max_seqs and capacity need: refused by the binding
+    short = kr.KVCache(cache.buf[:-16], cache.max_seqs, cache.capacity)
+    with pytest.raises(ValueError, match="cache holds"):
+        model.decode(X[:2], [0, 0], short)
+    # input and output buffers of the wrong type, size or device: refused by the binding
+    with pytest.raises(ValueError, match="dtype"):
+        model.decode(X[:2].float(), [0, 0], cache)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        model.prefill(X.cpu(), [0, 8])
+    with pytest.raises(ValueError, match="elements"):
+        model.prefill(X, [0, 4])
+    with pytest.raises(ValueError, match="elements"):
+        model.prefill(X, [0, 8], out=torch.empty((4, w.d_model), device=DEV))
     # the cache overlapping an output
     out = cache.buf.view(torch.float32)[: 2 * w.d_model].view(2, w.d_model)
     assert status(lambda: model.decode(X[:2], [0, 0], cache, out=out)) == kr.ERR_INVALID_ARG

@@ -342,6 +342,131 @@ def test_attention_large_logits_stay_finite():
                     "attention large logits")
 
 
+# ------------------------------------------- attention with pre-scaled Q (the product form)
+
+LOG2E = 1.4426950408889634
+
+PRESCALED_CASES = [  # (n, d, heads, seq_lens, heads checked per sub-layer or None = all)
+    (2, 256, 2, [300, 1, 129], None),            # head size 128: ping-pong kernel
+    (1, 512, 8, [513, 64], None),                # head size 64: one-phase kernel, scale 1
+    (2, 128, 4, [200, 7], None),                 # head size 32
+    (2, 1024, 8, [4500, 700], None),             # 71 + 11 key tiles, ragged tail
+    # the benchmark's attention launch for 4 of its 8 sub-layers: one 8192-token sequence,
+    # 16 heads of 128, 2048 workgroups in the head-grouped XCD order, all 128 key tiles
+    (4, 2048, 16, [8192], [0, 5, 10, 15]),
+    # ragged lengths of the packed 8-sequence workload at head size 128: the grouped order
+    # over an uneven tile prefix
+    (4, 2048, 16, [3585, 2177, 3101, 3452, 1119, 2039, 1665, 1442], [0, 9, 15]),
+]
+
+
+def prescaled_inputs(n, d, H, T, dt, seed):
+    """Q|K rows and V^T as the prefill hands them to attention: the Q columns carry
+    log2(e) / sqrt(hd) (rounded once to the operand type).  Returns the device operands and
+    the fp64 Q, K, V the oracle takes (Q divided back by the factor, exactly in fp64)."""
+    hd = d // H
+    c = LOG2E / math.sqrt(hd)
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((n, T, d), generator=g) * 1.5
+    k = torch.randn((n, T, d), generator=g) * 1.5
+    v = torch.randn((n, T, d), generator=g)
+    qk = torch.cat([(q * c).to(dt), k.to(dt)], dim=2)
+    v = v.to(dt)
+    ldv = K().vt_ld(T)
+    vt = torch.zeros((n, d, ldv), dtype=dt)
+    vt[:, :, :T] = v.transpose(1, 2)
+    q64 = qk[:, :, :d].double().numpy() / c
+    return qk, vt, q64, qk[:, :, d:].double().numpy(), v.double().numpy()
+
+
+def check_heads(got, q64, k64, v64, cu, H, heads, dtype, what):
+    """The kernel's output against the oracle's causal attention, for the given heads
+    (each head is independent: the oracle runs on those heads' columns alone)."""
+    hd = q64.shape[1] // H
+    heads = list(range(H)) if heads is None else heads
+    cols = np.concatenate([np.arange(h * hd, (h + 1) * hd) for h in heads])
+    qs, ks, vs = q64[:, cols], k64[:, cols], v64[:, cols]
+    ref = O.causal_attention(qs, ks, vs, cu, len(heads))
+    check_attention(got[:, cols], ref, np.concatenate([qs, ks], axis=1), np.abs(vs), cu,
+                    len(heads), dtype, what)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", PRESCALED_CASES)
+def test_attention_prescaled_q(dtype, case):
+    n, d, H, lens, heads = case
+    if heads is not None and dtype == "bf16":
+        heads = heads[:2]
+    cu = [0]
+    for s_ in lens:
+        cu.append(cu[-1] + s_)
+    T = cu[-1]
+    print(f"[attention q_prescaled] n={n} d={d} H={H} lens={lens} {dtype}", flush=True)
+    qk, vt, q64, k64, v64 = prescaled_inputs(n, d, H, T, tdt(dtype), T * 31 + d + n)
+    out = torch.full((n, T, d), float("nan"), dtype=tdt(dtype), device=DEV)
+    K().op_attention(qk.to(DEV), vt.to(DEV), out, n, d, H, cu, q_prescaled=True)
+    torch.cuda.synchronize()
+    got = f64(out)
+    for i in range(n):
+        check_heads(got[i], q64[i], k64[i], v64[i], cu, H, heads, dtype,
+                    f"pre-scaled attention sub-layer {i}")
+
+
+def test_attention_dma_base_with_bit31_of_the_low_address_word_set_and_clear():
+    """Regression test of a fixed fault.  The ping-pong attention kernel rebuilds each
+    wave-uniform 64-bit DMA base from two 32-bit halves; the low half must be widened as
+    unsigned, or an address whose low word has bit 31 set sign-extends over the high word.
+    Whether a tile base has that bit set depends on where the allocator puts the operands,
+    so here they are placed inside one allocation of more than 2 GiB at addresses whose low
+    word has bit 31 set, then clear, and the result is checked against the oracle."""
+    n, d, H, lens = 2, 256, 2, [1000, 300]
+    cu = [0, 1000, 1300]
+    T = cu[-1]
+    dt = torch.float16
+    qk, vt, q64, k64, v64 = prescaled_inputs(n, d, H, T, dt, 4242)
+    sizes = [qk.numel() * 2, vt.numel() * 2, n * T * d * 2]
+    offs = [0]
+    for sz in sizes[:-1]:
+        offs.append(offs[-1] + (sz + 4095) // 4096 * 4096)
+    need = offs[-1] + sizes[-1]
+    big = torch.empty(2 ** 31 + 2 * need + 8192, dtype=torch.uint8, device=DEV)
+    base = big.data_ptr()
+    for bit in (1, 0):
+        # first 4 KiB-aligned window of `need` bytes whose addresses all have bit 31 == bit
+        a = (base + 4095) // 4096 * 4096
+        if ((a >> 31) & 1) != bit or (((a + need - 1) >> 31) & 1) != bit:
+            a = ((a >> 31) + 1) << 31
+            if ((a >> 31) & 1) != bit:
+                a = ((a >> 31) + 1) << 31
+        assert a + need <= base + big.numel()
+        assert ((a >> 31) & 1) == bit and (((a + need - 1) >> 31) & 1) == bit
+        o = a - base
+        views = []
+        for off, sz, shape in zip(offs, sizes, [qk.shape, vt.shape, (n, T, d)]):
+            views.append(big[o + off:o + off + sz].view(dt).view(shape))
+        views[0].copy_(qk.to(DEV))
+        views[1].copy_(vt.to(DEV))
+        views[2].fill_(float("nan"))
+        for pre in (True, False):
+            if pre:          # the Q columns carry log2(e) / sqrt(hd)
+                q_ref = q64
+            else:            # plain Q: the operand holds unscaled values
+                plain = torch.from_numpy(q64).to(dt)
+                views[0][:, :, :d].copy_(plain.to(DEV))
+                q_ref = plain.double().numpy()
+            print(f"[attention dma base] low-word bit 31 = {bit}, q_prescaled={pre}",
+                  flush=True)
+            K().op_attention(views[0], views[1], views[2], n, d, H, cu, q_prescaled=pre)
+            torch.cuda.synchronize()
+            got = f64(views[2])
+            for i in range(n):
+                check_heads(got[i], q_ref[i], k64[i], v64[i], cu, H, None, "f16",
+                            f"bit31={bit} pre={pre} sub-layer {i}")
+    del big
+    torch.cuda.empty_cache()
+
+
 # ----------------------------------------------------------------------- decode attention
 
 DECODE_ATTN_CASES = [

@@ -3,14 +3,20 @@
 Metric: max |gpu - oracle| / RMS(oracle), over ``out`` [T, d] and ``sub_out``
 [N, T, d]; bound 2e-2 for bf16 storage and 1e-4 for fp32 storage.
 
-Small workloads are checked in full.  At the full benchmark sizes the oracle
-cannot run every token in a test's time, so it runs a causal prefix of every
-sequence (exact by causality and packing: earlier tokens never see later ones,
-sequences never see each other) at the full depth and width, and that is
-compared with the same rows of the full-length GPU run.
+Small workloads, and the N=4, L=12, d=768 workload, are checked in full.  For the
+larger benchmark workloads the oracle cannot run every token at the full depth in
+a test's time, so two checks replace the full run: the full-length run at a
+reduced depth of two layers, every row compared; and the full-depth run of
+which the oracle computes a causal prefix of every sequence (exact by causality
+and packing: earlier tokens never see later ones, sequences never see each
+other), compared with the same rows of the full-length GPU run.
+
+Every model call is followed by ``sync()``, which also asserts that no activation
+overflowed the fp16 operand range (no false alarm of the overflow check).
 """
 
 import dataclasses
+import os
 import sys
 
 import numpy as np
@@ -57,8 +63,10 @@ def build_model(w, T, seed=0, affine="plain"):
     return model
 
 
-def oracle_layers(w, seed=0, affine="plain"):
+def oracle_layers(w, seed=0, affine="plain", progress=False):
     for j in range(w.n_layers):
+        if progress and (j % 4 == 0 or w.n_layers <= 4):
+            say(f"      oracle layer {j + 1}/{w.n_layers}")
         yield [{k: f64(v) for k, v in sub.items()}
                for sub in synth.gen_layer(w, j, seed, DEV, affine)]
 
@@ -76,8 +84,9 @@ def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
         f"prefix={prefix}")
     model = build_model(w, T, seed, affine)
     X = synth.gen_hidden(w, T, seed, DEV)
+    model.poison_workspace()          # nothing may be read that this call did not write
     out, sub = model.prefill(X, cu, sub_out=True)
-    torch.cuda.synchronize()
+    model.sync()
     model.close()
     assert torch.isfinite(out).all() and torch.isfinite(sub).all()
     if prefix is None:
@@ -88,7 +97,8 @@ def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
                                for b in range(len(lens))])
         cu_o = synth.cu_seqlens([min(prefix, s) for s in lens])
     Xo = f64(X)[rows]
-    out_o, sub_o = O.kraken_prefill(Xo, cu_o, oracle_layers(w, seed, affine),
+    say(f"    oracle on {len(rows)} rows x {w.n_layers} layers")
+    out_o, sub_o = O.kraken_prefill(Xo, cu_o, oracle_layers(w, seed, affine, progress=True),
                                     f64(synth.gen_w_concat(w, seed, DEV)), w.n_heads,
                                     n_kv_heads=w.kv_heads)
     e_out = rel_err(f64(out)[rows], out_o)
@@ -165,9 +175,11 @@ def test_grouped_query_attention(dtype, H, Hkv, d):
 
 # ------------------------------------------------------- benchmark-size workloads, prefix
 
-def test_n4_l12_d768_s2048_prefix():
+@pytest.mark.timeout(900)
+def test_n4_l12_d768_s2048_every_row():
+    # the whole workload: every row of out and sub_out at the full depth
     w = synth.workload("kraken-n4-l12-d768-h12-s2048-bf16")
-    run_and_compare(w, synth.seq_lens(w), prefix=384)
+    run_and_compare(w, synth.seq_lens(w))
 
 
 def test_n4_l12_d768_s2048_random_affine_prefix():
@@ -175,14 +187,33 @@ def test_n4_l12_d768_s2048_random_affine_prefix():
     run_and_compare(w, synth.seq_lens(w), affine="random", prefix=192)
 
 
+@pytest.mark.timeout(900)
 def test_n4_l24_d1024_s4096_prefix():
     w = synth.workload("kraken-n4-l24-d1024-h16-s4096-bf16")
-    run_and_compare(w, synth.seq_lens(w), prefix=192)
+    run_and_compare(w, synth.seq_lens(w), prefix=1024)
 
 
+@pytest.mark.timeout(900)
+def test_n4_l24_d1024_s4096_two_layers_every_row():
+    w = dataclasses.replace(synth.workload("kraken-n4-l24-d1024-h16-s4096-bf16"), n_layers=2)
+    run_and_compare(w, synth.seq_lens(w))
+
+
+@pytest.mark.timeout(900)
 def test_n8_l24_d2048_s8192_prefix():
+    # full depth; the oracle runs the first 1024 of the 8192 tokens
     w = synth.workload("kraken-n8-l24-d2048-h16-s8192-bf16")
-    run_and_compare(w, synth.seq_lens(w), prefix=96)
+    run_and_compare(w, synth.seq_lens(w), prefix=1024)
+
+
+@pytest.mark.timeout(900)
+def test_n8_d2048_s8192_two_layers_every_row():
+    """The benchmark's launch configuration at reduced depth: N=8, d=2048, 16 heads of 128,
+    one 8192-token sequence, fp16 operands, so attention is the ping-pong kernel with
+    pre-scaled Q in the head-grouped workgroup order over all 128 key tiles.  Every one of
+    the 8192 rows of out and sub_out is compared with the oracle."""
+    w = dataclasses.replace(synth.workload("kraken-n8-l24-d2048-h16-s8192-bf16"), n_layers=2)
+    run_and_compare(w, synth.seq_lens(w))
 
 
 def test_n8_l24_d2048_s8192_first_half_equals_4096_token_prefill():
@@ -193,8 +224,11 @@ def test_n8_l24_d2048_s8192_first_half_equals_4096_token_prefill():
     model = build_model(w, 8192)
     X = synth.gen_hidden(w, 8192, 0, DEV)
     out_f, sub_f = model.prefill(X, [0, 8192], sub_out=True)
+    # the first call left rows 0..4095 of every intermediate exactly as the second must
+    # write them: poison the workspace so that a row the second call fails to write shows
+    model.poison_workspace()
     out_h, sub_h = model.prefill(X[:4096].contiguous(), [0, 4096], sub_out=True)
-    torch.cuda.synchronize()
+    model.sync()
     model.close()
     e_out = rel_err(f64(out_f[:4096]), f64(out_h))
     e_sub = rel_err(f64(sub_f[:, :4096]), f64(sub_h))
@@ -202,9 +236,19 @@ def test_n8_l24_d2048_s8192_first_half_equals_4096_token_prefill():
     assert e_out <= 1e-6 and e_sub <= 1e-6
 
 
+@pytest.mark.timeout(900)
 def test_n4_l36_d1280_ragged8_prefix():
+    # full depth; the oracle runs the first 512 tokens of each of the 8 sequences
     w = synth.workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16")
-    run_and_compare(w, synth.seq_lens(w), prefix=40)
+    run_and_compare(w, synth.seq_lens(w), prefix=512)
+
+
+@pytest.mark.timeout(900)
+def test_n4_d1280_ragged8_two_layers_every_row():
+    # all 8 sequences at their full lengths (T = 18580), every row, two layers
+    w = dataclasses.replace(synth.workload("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16"),
+                            n_layers=2)
+    run_and_compare(w, synth.seq_lens(w))
 
 
 # ------------------------------------------------------------------- GPU invariants
@@ -215,9 +259,11 @@ def test_run_to_run_bitwise_determinism_and_prefix_invariance():
     model = build_model(w, 300, affine="random")
     X = synth.gen_hidden(w, 300, 0, DEV)
     out1, sub1 = model.prefill(X, [0, 300], sub_out=True)
+    model.poison_workspace()          # (no result may come from the previous call's rows)
     out2, sub2 = model.prefill(X, [0, 300], sub_out=True)
+    model.poison_workspace()
     outp, subp = model.prefill(X[:133].contiguous(), [0, 133], sub_out=True)
-    torch.cuda.synchronize()
+    model.sync()
     assert torch.equal(out1, out2) and torch.equal(sub1, sub2)
     # rows never depend on later tokens: the same kernels give the same bits on a prefix
     assert torch.equal(outp, out1[:133]) and torch.equal(subp, sub1[:, :133])
@@ -323,4 +369,102 @@ def test_fp16_operand_overflow_is_rejected_at_load():
     with pytest.raises(K().KrakenError) as ei:      # the model stays unloaded
         model.prefill(X, [0, 8])
     assert ei.value.status == K().ERR_STATE
+    model.close()
+
+
+# ----------------------------------------------------- workspace poison, debug sync, overflow
+
+POISON_SHAPES = [  # (name, n_sub, d, heads, kv heads, d_ff, dtype, compute, lens)
+    ("poison-hd64-f32", 3, 256, 4, 0, 512, "f32", "storage", [1, 130, 77, 300]),
+    ("poison-hd128-f16", 2, 256, 2, 0, 512, "bf16", "f16", [200, 33, 513]),
+    ("poison-hd32-bf16", 2, 128, 4, 0, 256, "bf16", "storage", [96, 5]),
+    ("poison-gqa-f16", 2, 512, 4, 2, 1024, "bf16", "f16", [300, 64, 1]),
+]
+
+
+@pytest.mark.parametrize("shape", POISON_SHAPES, ids=[p[0] for p in POISON_SHAPES])
+def test_poisoned_workspace_gives_identical_results(shape):
+    """A prefill after the whole workspace was filled with NaN bytes is bit-identical to one
+    after a normal prefill: every workspace element a kernel reads (the V^T padding
+    columns included) is written earlier in the same call."""
+    name, n, d, H, Hkv, F, dtype, compute, lens = shape
+    w = small(name, n_sub=n, n_layers=2, d_model=d, n_heads=H, d_ff=F, dtype=dtype,
+              compute=compute, n_kv_heads=Hkv)
+    cu = synth.cu_seqlens(lens)
+    T = cu[-1]
+    say(f"[poison] {name} lens={lens}")
+    model = build_model(w, T + 100, affine="random")
+    X = synth.gen_hidden(w, T, 0, DEV)
+    big = synth.gen_hidden(w, T + 100, 1, DEV)
+    model.prefill(big, [0, T + 100])             # leaves a longer call's values everywhere
+    out1, sub1 = model.prefill(X, cu, sub_out=True)
+    model.poison_workspace()
+    out2, sub2 = model.prefill(X, cu, sub_out=True)
+    model.sync()
+    assert torch.isfinite(out2).all() and torch.isfinite(sub2).all()
+    assert torch.equal(out1, out2) and torch.equal(sub1, sub2)
+    model.close()
+
+
+def test_debug_sync_mode_is_bit_identical():
+    """KRAKEN_DEBUG_SYNC=1 synchronises and checks after every launch; the results are the
+    same bits as a normal run."""
+    w = small("debug-sync", n_sub=2, n_layers=2, d_model=256, n_heads=2, d_ff=512,
+              compute="f16")
+    lens = [130, 7]
+    cu = synth.cu_seqlens(lens)
+    X = synth.gen_hidden(w, cu[-1], 0, DEV)
+    normal = build_model(w, cu[-1], affine="random")
+    o1, s1 = normal.prefill(X, cu, sub_out=True)
+    normal.sync()
+    old = os.environ.get("KRAKEN_DEBUG_SYNC")
+    os.environ["KRAKEN_DEBUG_SYNC"] = "1"
+    try:
+        dbg = build_model(w, cu[-1], affine="random")
+    finally:
+        if old is None:
+            del os.environ["KRAKEN_DEBUG_SYNC"]
+        else:
+            os.environ["KRAKEN_DEBUG_SYNC"] = old
+    o2, s2 = dbg.prefill(X, cu, sub_out=True)
+    dbg.sync()
+    assert torch.equal(o1, o2) and torch.equal(s1, s2)
+    normal.close()
+    dbg.close()
+
+
+def _overflow_model(compute, gamma):
+    w = small("overflow-act", n_sub=2, n_layers=2, d_model=128, n_heads=2, d_ff=256,
+              compute=compute)
+    cfg = cfg_of(w, 64)
+    layers = [synth.gen_layer(w, j, 0, DEV) for j in range(2)]
+    layers[1][1]["ln1_g"].fill_(gamma)   # an LN1 output of about gamma * N(0, 1)
+    blob = K().pack_weights(layers, synth.gen_w_concat(w, 0, DEV), cfg, device=DEV)
+    model = K().Kraken(cfg)
+    model.load_weights(blob)
+    return w, model
+
+
+def test_fp16_activation_overflow_is_reported():
+    """A LayerNorm gain of 1e5 (representable in bf16, loaded as an fp32 parameter) puts the
+    LayerNorm output past the fp16 range: with fp16 operands kraken_sync reports
+    KRAKEN_ERR_OVERFLOW, once (the flag is cleared), and a following normal call is clean."""
+    w, model = _overflow_model("f16", 1.0e5)
+    X = synth.gen_hidden(w, 64, 0, DEV)
+    model.prefill(X, [0, 64])
+    with pytest.raises(K().KrakenError) as ei:
+        model.sync()
+    assert ei.value.status == K().ERR_OVERFLOW
+    model.sync()                                 # cleared by the report
+    model.close()
+    # the same model with bf16 operands has the fp32 exponent range: no overflow
+    w, model = _overflow_model("bf16", 1.0e5)
+    out, _ = model.prefill(X, [0, 64])
+    model.sync()
+    assert torch.isfinite(out).all()
+    model.close()
+    # a gain just inside the range: no report
+    w, model = _overflow_model("f16", 1.0)
+    model.prefill(X, [0, 64])
+    model.sync()
     model.close()
