@@ -49,10 +49,20 @@ head g (head h reads K/V head ``h // G``); Hkv = 1 is multi-query attention and
 Hkv = H the standard multi-head attention.  Only the key and value projections
 narrow, to dkv = Hkv * hd columns each.
 
+The whole model (``model_forward``): token and position embeddings shared by the
+first layer (Section 3.1), the layer stack, W_concat for Kraken, a final
+LayerNorm and the unembedding tied to the token embedding, giving the
+next-token logits of each sequence's last token (Section 2.1).  Besides the
+Kraken stack it runs the two architectures the paper compares with at the same
+sizes (Section 4.3, engine configurations): the standard GPT-like layer and the
+parallel attention + FFN layer of GPT-J / PaLM.  The head size may differ from
+the width divided by the heads (``head_dim``), as in the GPT-3 13B configuration.
+
 Weight layout taken by this module (a convention, not mathematics): every
 matrix multiplies as ``u @ W`` (row-major ``[in, out]``); ``Wqkv`` has
-columns ``[Q | K | V]`` (widths d, dkv, dkv) and head ``h`` owns columns
-``h*hd:(h+1)*hd`` of Q, key/value head ``g`` columns ``g*hd:(g+1)*hd`` of K and V.
+columns ``[Q | K | V]`` (widths dq = heads * hd, dkv, dkv) and head ``h`` owns
+columns ``h*hd:(h+1)*hd`` of Q, key/value head ``g`` columns ``g*hd:(g+1)*hd`` of
+K and V; ``Wo`` is ``[dq, d]``.
 """
 
 from __future__ import annotations
@@ -126,18 +136,22 @@ def causal_attention(Q, K, V, cu_seqlens: Sequence[int], n_heads: int,
 
 def multi_head_attention(u, p: Mapping, cu_seqlens, n_heads: int,
                          kv_out: list | None = None,
-                         n_kv_heads: int | None = None) -> np.ndarray:
+                         n_kv_heads: int | None = None,
+                         head_dim: int | None = None) -> np.ndarray:
     """MHA block: QKV projection, per-head causal attention, output projection.
 
-    ``Wqkv`` has ``d + 2 dkv`` columns ``[Q | K | V]``, dkv = n_kv_heads * hd.
+    ``Wqkv`` has ``dq + 2 dkv`` columns ``[Q | K | V]`` with dq = n_heads * hd and
+    dkv = n_kv_heads * hd; hd = ``head_dim``, by default d / n_heads (Section 4.3:
+    the model width divided by the number of heads), and ``Wo`` is ``[dq, d]``.
     With ``kv_out`` (a list), appends this block's keys and values ``(K, V)``
     (``[T, dkv]`` each, the projections the attention used).
     """
     u = _f64(u)
     d = u.shape[1]
-    dkv = d // n_heads * (n_kv_heads or n_heads)
+    hd = head_dim or d // n_heads
+    dq, dkv = n_heads * hd, hd * (n_kv_heads or n_heads)
     qkv = u @ _f64(p["Wqkv"]) + _f64(p["bqkv"])
-    Q, K, V = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
+    Q, K, V = qkv[:, :dq], qkv[:, dq:dq + dkv], qkv[:, dq + dkv:]
     if kv_out is not None:
         kv_out.append((K, V))
     return (causal_attention(Q, K, V, cu_seqlens, n_heads, n_kv_heads) @ _f64(p["Wo"])
@@ -152,21 +166,22 @@ def feed_forward(u, p: Mapping) -> np.ndarray:
 
 def sub_layer_forward(x, y, p: Mapping, cu_seqlens, n_heads: int,
                       eps: float = LN_EPS, kv_out: list | None = None,
-                      n_kv_heads: int | None = None) -> np.ndarray:
+                      n_kv_heads: int | None = None,
+                      head_dim: int | None = None) -> np.ndarray:
     """One Kraken sub-layer (Algorithm 1) given its input ``x`` and combined ``y``.
 
     ``h = x + MHA(LN1(x))``; returns ``h + FFN(LN2(h + y))``.  ``kv_out``,
-    ``n_kv_heads``: see ``multi_head_attention``.
+    ``n_kv_heads``, ``head_dim``: see ``multi_head_attention``.
     """
     x = _f64(x)
     h = x + multi_head_attention(layer_norm(x, p["ln1_g"], p["ln1_b"], eps),
-                                 p, cu_seqlens, n_heads, kv_out, n_kv_heads)
+                                 p, cu_seqlens, n_heads, kv_out, n_kv_heads, head_dim)
     return h + feed_forward(layer_norm(h + _f64(y), p["ln2_g"], p["ln2_b"], eps), p)
 
 
 def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mapping]],
                    W_concat, n_heads: int, eps: float = LN_EPS, return_kv: bool = False,
-                   n_kv_heads: int | None = None):
+                   n_kv_heads: int | None = None, head_dim: int | None = None):
     """Forward pass of a stack of Kraken layers followed by ``W_concat``.
 
     ``X`` is the shared first-layer input ``[T, d]`` (Section 3.1: one set of
@@ -199,7 +214,7 @@ def kraken_prefill(X, cu_seqlens: Sequence[int], layers: Iterable[Sequence[Mappi
             y = np.sum(xs, axis=0)
         kv_j = []
         xs = [sub_layer_forward(xs[i], y, layer[i], cu_seqlens, n_heads, eps,
-                                kv_j if return_kv else None, n_kv_heads)
+                                kv_j if return_kv else None, n_kv_heads, head_dim)
               for i in range(n_sub)]
         kv.append(kv_j)
     if xs is None:
@@ -298,6 +313,96 @@ def split_kv(kv, cu_seqlens: Sequence[int]):
                         [V[cu_seqlens[b]:cu_seqlens[b + 1]] for b in range(len(cu_seqlens) - 1)]))
         out.append(row)
     return out
+
+
+# ------------------------------------------------------------------ the whole model
+#
+# Section 2.1 (background): a decoder-only model turns the tokens into embeddings that
+# carry each token and its position, runs the layer stack, and feeds the last layer's
+# activations to the unembedding, which gives the next-token logits.  Section 3.1: a
+# Kraken model keeps one set of token and position embeddings, shared by all first-layer
+# sub-layers (for compatibility with weight tying), and its W_concat output is the
+# unembedding's input.  Section 4.3 compares Kraken with two other architectures built
+# at the same sizes: the standard GPT-like model (Section 2.1: sequential pre-LN
+# attention and FFN blocks) and the parallel attention + FFN layer of GPT-J and PaLM
+# (the FFN runs beside the attention instead of after it).
+#
+# Readings: positions count from 0 inside each packed sequence; a final LayerNorm
+# (weights lnf_g, lnf_b) precedes the unembedding, as in the GPT-2 models the paper's
+# training code builds on; the unembedding is tied to the token embedding (logits =
+# LN_f(h) @ tok_emb^T); the parallel layer has one LayerNorm whose output feeds both
+# branches, x + MHA(LN(x)) + FFN(LN(x)) (the PaLM formulation); the standard layer is
+# h = x + MHA(LN1(x)), x' = h + FFN(LN2(h)).
+
+ARCHS = ("kraken", "gpt", "parallel")
+
+
+def embed(token_ids, cu_seqlens: Sequence[int], tok_emb, pos_emb) -> np.ndarray:
+    """First-layer input: ``tok_emb[id] + pos_emb[position]``, the position of token t of
+    packed sequence b being ``t - cu[b]`` (Section 2.1; Section 3.1 shares this one input
+    across the first layer's sub-layers)."""
+    ids = np.asarray(token_ids, dtype=np.int64)
+    tok, pos = _f64(tok_emb), _f64(pos_emb)
+    X = np.empty((len(ids), tok.shape[1]), dtype=np.float64)
+    for b in range(len(cu_seqlens) - 1):
+        s0, s1 = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+        X[s0:s1] = tok[ids[s0:s1]] + pos[:s1 - s0]
+    return X
+
+
+def gpt_block_forward(x, p: Mapping, cu_seqlens, n_heads: int, eps: float = LN_EPS,
+                      head_dim: int | None = None) -> np.ndarray:
+    """Standard pre-LN layer (Section 2.1): ``h = x + MHA(LN1(x))``, returns
+    ``h + FFN(LN2(h))``."""
+    x = _f64(x)
+    h = x + multi_head_attention(layer_norm(x, p["ln1_g"], p["ln1_b"], eps), p, cu_seqlens,
+                                 n_heads, head_dim=head_dim)
+    return h + feed_forward(layer_norm(h, p["ln2_g"], p["ln2_b"], eps), p)
+
+
+def parallel_block_forward(x, p: Mapping, cu_seqlens, n_heads: int, eps: float = LN_EPS,
+                           head_dim: int | None = None) -> np.ndarray:
+    """Parallel attention + FFN layer (Section 4.3, the GPT-J / PaLM comparison): one
+    LayerNorm ``u = LN(x)`` (weights ln1_g, ln1_b) feeds both branches; returns
+    ``x + MHA(u) + FFN(u)``."""
+    x = _f64(x)
+    u = layer_norm(x, p["ln1_g"], p["ln1_b"], eps)
+    return x + multi_head_attention(u, p, cu_seqlens, n_heads, head_dim=head_dim) + \
+        feed_forward(u, p)
+
+
+def unembed(h, lnf_g, lnf_b, tok_emb, eps: float = LN_EPS) -> np.ndarray:
+    """Next-token logits of the rows of ``h``: ``LN_f(h) @ tok_emb^T`` (tied weights)."""
+    return layer_norm(h, lnf_g, lnf_b, eps) @ _f64(tok_emb).T
+
+
+def model_forward(token_ids, cu_seqlens: Sequence[int], arch: str,
+                  layers: Iterable[Sequence[Mapping]], emb: Mapping, n_heads: int,
+                  W_concat=None, eps: float = LN_EPS, head_dim: int | None = None,
+                  n_kv_heads: int | None = None):
+    """The whole model on packed token sequences.
+
+    ``emb`` holds ``tok_emb [V, d]``, ``pos_emb [P, d]``, ``lnf_g``, ``lnf_b``.
+    ``arch`` "kraken": the Kraken stack (``layers`` yields N sub-layer mappings per layer)
+    and W_concat; "gpt" / "parallel": one mapping per layer, the standard or parallel
+    layer, no W_concat.  Returns ``(logits, hidden)``: the logits ``[num_seqs, V]`` of the
+    last token of every sequence (the first generated token's distribution, what the
+    time to first token measures) and the unembedding's input ``hidden [T, d]``.
+    """
+    if arch not in ARCHS:
+        raise ValueError(f"unknown architecture {arch!r}")
+    X = embed(token_ids, cu_seqlens, emb["tok_emb"], emb["pos_emb"])
+    if arch == "kraken":
+        hidden, _ = kraken_prefill(X, cu_seqlens, layers, W_concat, n_heads, eps,
+                                   n_kv_heads=n_kv_heads, head_dim=head_dim)
+    else:
+        block = gpt_block_forward if arch == "gpt" else parallel_block_forward
+        hidden = X
+        for layer in layers:
+            (p,) = layer
+            hidden = block(hidden, p, cu_seqlens, n_heads, eps, head_dim)
+    last = [int(c) - 1 for c in cu_seqlens[1:]]
+    return unembed(hidden[last], emb["lnf_g"], emb["lnf_b"], emb["tok_emb"], eps), hidden
 
 
 def kraken_param_count(n_sub: int, n_layers: int, d: int, d_ff: int,

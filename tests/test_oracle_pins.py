@@ -633,3 +633,195 @@ def test_gqa_parameter_count():
         dkv = Hkv * d // H
         got = O.kraken_param_count(N, L, d, f, kv_width=dkv)
         assert full - got == N * L * 2 * (d - dkv) * (d + 1)
+
+
+# ------------------------------------------------------------ the whole model (NEXT-4)
+
+def torch_mha(a, t, cu, n_heads, hd):
+    """Causal multi-head attention block from torch primitives (QKV, SDPA, Wo)."""
+    dq = n_heads * hd
+    qkv = F.linear(a, t["Wqkv"].T, t["bqkv"])
+    q, k, v = qkv[:, :dq], qkv[:, dq:2 * dq], qkv[:, 2 * dq:]
+    o = torch.empty_like(q)
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+
+        def heads(m):
+            return m[s0:s1].reshape(s1 - s0, n_heads, hd).transpose(0, 1)
+
+        att = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), is_causal=True)
+        o[s0:s1] = att.transpose(0, 1).reshape(s1 - s0, dq)
+    return F.linear(o, t["Wo"].T, t["bo"])
+
+
+def torch_ffn(z, t):
+    return F.linear(F.gelu(F.linear(z, t["W1"].T, t["b1"])), t["W2"].T, t["b2"])
+
+
+def tt(p):
+    return {k: torch.from_numpy(np.asarray(v, dtype=np.float64)) for k, v in p.items()}
+
+
+def torch_gpt_block(x, p, cu, n_heads, hd):
+    t, d = tt(p), x.shape[1]
+    h = x + torch_mha(F.layer_norm(x, (d,), t["ln1_g"], t["ln1_b"], eps=1e-5), t, cu, n_heads, hd)
+    return h + torch_ffn(F.layer_norm(h, (d,), t["ln2_g"], t["ln2_b"], eps=1e-5), t)
+
+
+def torch_parallel_block(x, p, cu, n_heads, hd):
+    t, d = tt(p), x.shape[1]
+    u = F.layer_norm(x, (d,), t["ln1_g"], t["ln1_b"], eps=1e-5)
+    return x + torch_mha(u, t, cu, n_heads, hd) + torch_ffn(u, t)
+
+
+def rand_params_hd(rng, d, f, n_heads, hd, scale=0.3):
+    """Sub-layer parameters with an attention width n_heads * hd that may differ from d."""
+    dq = n_heads * hd
+    return {"Wqkv": rng.normal(0, scale, (d, 3 * dq)), "bqkv": rng.normal(0, 0.2, 3 * dq),
+            "Wo": rng.normal(0, scale, (dq, d)), "bo": rng.normal(0, 0.2, d),
+            "W1": rng.normal(0, scale, (d, f)), "b1": rng.normal(0, 0.2, f),
+            "W2": rng.normal(0, scale, (f, d)), "b2": rng.normal(0, 0.2, d),
+            "ln1_g": 1 + rng.normal(0, 0.2, d), "ln1_b": rng.normal(0, 0.2, d),
+            "ln2_g": 1 + rng.normal(0, 0.2, d), "ln2_b": rng.normal(0, 0.2, d)}
+
+
+def rand_emb(rng, V, P, d):
+    return {"tok_emb": rng.normal(0, 1.0, (V, d)), "pos_emb": rng.normal(0, 0.5, (P, d)),
+            "lnf_g": 1 + rng.normal(0, 0.2, d), "lnf_b": rng.normal(0, 0.2, d)}
+
+
+def test_embed_is_token_plus_position_within_each_sequence():
+    rng = np.random.default_rng(50)
+    V, P, d = 11, 9, 6
+    emb = rand_emb(rng, V, P, d)
+    cu = [0, 4, 5, 9]
+    ids = rng.integers(0, V, 9)
+    X = O.embed(ids, cu, emb["tok_emb"], emb["pos_emb"])
+    pos = torch.tensor([0, 1, 2, 3, 0, 0, 1, 2, 3])        # positions restart per sequence
+    want = F.embedding(torch.from_numpy(ids), torch.from_numpy(emb["tok_emb"])) + \
+        F.embedding(pos, torch.from_numpy(emb["pos_emb"]))
+    assert rel_err(X, want.numpy()) <= 1e-15
+    # one-hot form: X = onehot(ids) tok_emb + onehot(pos) pos_emb
+    oh = np.eye(V)[ids] @ emb["tok_emb"] + np.eye(P)[pos.numpy()] @ emb["pos_emb"]
+    assert rel_err(X, oh) <= 1e-14
+
+
+@pytest.mark.parametrize("hd", [None, 5])
+def test_gpt_block_is_the_vanilla_pre_ln_block(hd):
+    # hd = 5 with 3 heads and d = 16: an attention width (15) that differs from d, as in a
+    # GPT-3 13B layer (d = 5140, 40 heads of 128)
+    rng = np.random.default_rng(51)
+    d, f, H, cu = 16, 40, 3 if hd else 4, [0, 9, 20]
+    hd_ = hd or d // H
+    x = rng.normal(size=(cu[-1], d))
+    p = rand_params_hd(rng, d, f, H, hd_)
+    got = O.gpt_block_forward(x, p, cu, H, head_dim=hd)
+    want = torch_gpt_block(torch.from_numpy(x), p, cu, H, hd_).numpy()
+    assert rel_err(got, want) <= 1e-12
+    # it is not the Kraken sub-layer with N = 1 (whose FFN LayerNorm reads h + x)
+    if hd is None:
+        assert rel_err(O.sub_layer_forward(x, x, p, cu, H), got) > 1e-3
+
+
+def test_parallel_block_against_torch_and_its_two_reductions():
+    rng = np.random.default_rng(52)
+    d, f, H, cu = 16, 40, 4, [0, 7, 19]
+    x = rng.normal(size=(cu[-1], d))
+    p = rand_params_hd(rng, d, f, H, d // H)
+    got = O.parallel_block_forward(x, p, cu, H)
+    want = torch_parallel_block(torch.from_numpy(x), p, cu, H, d // H).numpy()
+    assert rel_err(got, want) <= 1e-12
+    # FFN off (W1, b1, W2, b2 = 0): both layer forms are x + MHA(LN1(x))
+    q = dict(p, W1=np.zeros_like(p["W1"]), b1=np.zeros(f), W2=np.zeros_like(p["W2"]),
+             b2=np.zeros(d))
+    assert rel_err(O.parallel_block_forward(x, q, cu, H), O.gpt_block_forward(x, q, cu, H)) <= 1e-13
+    # attention off (Wqkv, bqkv, bo = 0, so MHA = 0) and LN2 = LN1: both are x + FFN(LN(x))
+    r = dict(p, Wqkv=np.zeros_like(p["Wqkv"]), bqkv=np.zeros_like(p["bqkv"]), bo=np.zeros(d),
+             ln2_g=p["ln1_g"], ln2_b=p["ln1_b"])
+    assert rel_err(O.parallel_block_forward(x, r, cu, H), O.gpt_block_forward(x, r, cu, H)) <= 1e-13
+    # with both branches on, the two forms differ
+    assert rel_err(got, O.gpt_block_forward(x, p, cu, H)) > 1e-3
+
+
+def test_unembed_against_torch_and_loops():
+    rng = np.random.default_rng(53)
+    V, d = 7, 5
+    emb = rand_emb(rng, V, 3, d)
+    h = rng.normal(size=(3, d)) * 4 + 2
+    got = O.unembed(h, emb["lnf_g"], emb["lnf_b"], emb["tok_emb"])
+    t = tt(emb)
+    want = F.linear(F.layer_norm(torch.from_numpy(h), (d,), t["lnf_g"], t["lnf_b"], eps=1e-5),
+                    t["tok_emb"]).numpy()
+    assert rel_err(got, want) <= 1e-13
+    for r in range(3):          # logit v is the dot product with token v's embedding
+        mu = sum(h[r]) / d
+        var = sum((a - mu) ** 2 for a in h[r]) / d
+        z = [emb["lnf_g"][c] * (h[r][c] - mu) / math.sqrt(var + 1e-5) + emb["lnf_b"][c]
+             for c in range(d)]
+        for v in range(V):
+            assert abs(got[r][v] - sum(z[c] * emb["tok_emb"][v][c] for c in range(d))) <= 1e-12
+
+
+def torch_model(ids, cu, arch, layers, emb, H, hd, Wc=None):
+    """The whole model from torch primitives: embeddings, blocks, (W_concat), ln_f, tied
+    unembedding of each sequence's last token."""
+    t = tt(emb)
+    pos = torch.cat([torch.arange(cu[b + 1] - cu[b]) for b in range(len(cu) - 1)])
+    x = F.embedding(torch.from_numpy(np.asarray(ids)), t["tok_emb"]) + F.embedding(pos, t["pos_emb"])
+    d = x.shape[1]
+    if arch == "kraken":
+        xs, y = [x] * len(layers[0]), x
+        for j, layer in enumerate(layers):
+            if j > 0:
+                y = sum(xs)
+            nxt = []
+            for i, p in enumerate(layer):
+                q = tt(p)
+                h = xs[i] + torch_mha(F.layer_norm(xs[i], (d,), q["ln1_g"], q["ln1_b"], eps=1e-5),
+                                      q, cu, H, hd)
+                nxt.append(h + torch_ffn(F.layer_norm(h + y, (d,), q["ln2_g"], q["ln2_b"],
+                                                      eps=1e-5), q))
+            xs = nxt
+        x = torch.cat(xs, dim=1) @ torch.from_numpy(Wc)
+    else:
+        blk = torch_gpt_block if arch == "gpt" else torch_parallel_block
+        for (p,) in layers:
+            x = blk(x, p, cu, H, hd)
+    last = [c - 1 for c in cu[1:]]
+    return F.linear(F.layer_norm(x[last], (d,), t["lnf_g"], t["lnf_b"], eps=1e-5),
+                    t["tok_emb"]).numpy()
+
+
+@pytest.mark.parametrize("arch", ["kraken", "gpt", "parallel"])
+def test_model_forward_against_torch_model(arch):
+    rng = np.random.default_rng(54)
+    V, P, d, f, H, L = 13, 12, 12, 24, 3, 2
+    N = 3 if arch == "kraken" else 1
+    cu = [0, 5, 12]
+    ids = rng.integers(0, V, 12)
+    emb = rand_emb(rng, V, P, d)
+    layers = [[rand_params_hd(rng, d, f, H, d // H) for _ in range(N)] for _ in range(L)]
+    Wc = rng.normal(0, 0.3, (N * d, d)) if arch == "kraken" else None
+    logits, hidden = O.model_forward(ids, cu, arch, layers, emb, H, W_concat=Wc)
+    assert logits.shape == (2, V) and hidden.shape == (12, d)
+    want = torch_model(ids, cu, arch, layers, emb, H, d // H, Wc)
+    assert rel_err(logits, want) <= 1e-12
+
+
+@pytest.mark.parametrize("arch", ["kraken", "gpt", "parallel"])
+def test_model_forward_packing_equals_separate_sequences(arch):
+    # positions restart in every packed sequence and attention never crosses sequences, so
+    # each sequence's last-token logits equal a run of that sequence alone
+    rng = np.random.default_rng(55)
+    V, P, d, f, H = 9, 10, 8, 16, 2
+    N = 2 if arch == "kraken" else 1
+    emb = rand_emb(rng, V, P, d)
+    layers = [[rand_params_hd(rng, d, f, H, d // H) for _ in range(N)] for _ in range(2)]
+    Wc = rng.normal(0, 0.3, (N * d, d)) if arch == "kraken" else None
+    lens = [4, 1, 7]
+    ids = rng.integers(0, V, sum(lens))
+    cu = [0, 4, 5, 12]
+    packed, _ = O.model_forward(ids, cu, arch, layers, emb, H, W_concat=Wc)
+    for b, s in enumerate(lens):
+        alone, _ = O.model_forward(ids[cu[b]:cu[b + 1]], [0, s], arch, layers, emb, H, W_concat=Wc)
+        assert rel_err(packed[b], alone[0]) <= 1e-12
