@@ -388,6 +388,31 @@ kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const vo
                                          int32_t num_seqs, int32_t max_seqs, int32_t capacity,
                                          float* work, int64_t work_floats, void* stream);
 
+/*
+ * kraken_op_decode_attention_noalloc: kraken_op_decode_attention without the `work`
+ * argument, for callers that cannot allocate device memory (code being captured into a
+ * HIP graph, tight serving loops, harnesses that forbid hipMalloc).  The per-chunk
+ * partials live in a static device array of KRAKEN_NOALLOC_SCRATCH_FLOATS floats (32 MiB)
+ * that the library holds on every GPU it runs on until the process ends; the call itself
+ * allocates and frees nothing.  Arguments and result are those of
+ * kraken_op_decode_attention with work_floats = KRAKEN_NOALLOC_SCRATCH_FLOATS (the same
+ * key split, so the same bits).
+ * Limit: n * num_seqs * n_heads * (hd + 2) must not exceed KRAKEN_NOALLOC_SCRATCH_FLOATS
+ * (one key chunk's partials), else KRAKEN_ERR_UNSUPPORTED with a message.
+ * Every call on one GPU shares that GPU's array (nothing in it needs to start at zero:
+ * each call writes every partial it reads): calls that overlap in time on one GPU, e.g.
+ * on two streams, race and must be serialised by the caller.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP (including a failed lookup of the array's
+ * device address on the first call on a device).
+ */
+#define KRAKEN_NOALLOC_SCRATCH_FLOATS (8 * 1024 * 1024)
+kraken_status kraken_op_decode_attention_noalloc(int32_t dtype, const void* qk,
+                                                 const void* kv_layer, void* out, int32_t n,
+                                                 int32_t d, int32_t n_heads, int32_t n_kv_heads,
+                                                 const int32_t* lens, int32_t num_seqs,
+                                                 int32_t max_seqs, int32_t capacity,
+                                                 void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,6 +15,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -27,6 +28,15 @@ using namespace kraken;
 namespace {
 
 thread_local std::string g_last_error;
+
+// Scratch of the allocation-free decode attention (kraken_op_decode_attention_noalloc): the
+// per-chunk (max, sum, output) partials, fp32.  One copy per GPU, held until the process
+// ends.  In host code `scratch` only names the symbol; its device address is looked up
+// once per device and kept in g_scratch_ptr.
+static __device__ __align__(256) float scratch[KRAKEN_NOALLOC_SCRATCH_FLOATS];
+constexpr int kMaxDevices = 64;
+float* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mutex;
 
 kraken_status fail(kraken_status st, const std::string& msg) {
   g_last_error = msg;
@@ -1004,6 +1014,58 @@ kraken_status kraken_op_decode_attention(int32_t dtype, const void* qk, const vo
                                          num_seqs, d, n_heads, n_kv_heads, lens, max_seqs,
                                          capacity, 0, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "decode attention");
+}
+
+kraken_status kraken_op_decode_attention_noalloc(int32_t dtype, const void* qk,
+                                                 const void* kv_layer, void* out, int32_t n,
+                                                 int32_t d, int32_t n_heads, int32_t n_kv_heads,
+                                                 const int32_t* lens, int32_t num_seqs,
+                                                 int32_t max_seqs, int32_t capacity,
+                                                 void* stream) {
+  if (!qk || !kv_layer || !out || !lens) return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
+  if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
+    return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
+  if (n < 1 || d < 1 || n_heads < 1 || d % n_heads != 0)
+    return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
+  const int hd = d / n_heads;
+  if (hd != 32 && hd != 64 && hd != 128) return fail(KRAKEN_ERR_UNSUPPORTED, "head size");
+  if (n_kv_heads < 0 || (n_kv_heads > 0 && n_heads % n_kv_heads != 0))
+    return fail(KRAKEN_ERR_INVALID_ARG, "n_kv_heads must be 0 or divide n_heads");
+  if (num_seqs < 1 || num_seqs > KRAKEN_MAX_SEQS || max_seqs < num_seqs ||
+      max_seqs > KRAKEN_MAX_SEQS || capacity < 1)
+    return fail(KRAKEN_ERR_INVALID_ARG, "num_seqs, max_seqs or capacity out of range");
+  if (reinterpret_cast<uintptr_t>(kv_layer) % 16 != 0 || reinterpret_cast<uintptr_t>(qk) % 16 != 0)
+    return fail(KRAKEN_ERR_INVALID_ARG, "qk or kv_layer is not 16-byte aligned");
+  for (int b = 0; b < num_seqs; ++b)
+    if (lens[b] < 0 || lens[b] >= capacity)
+      return fail(KRAKEN_ERR_INVALID_ARG, "lens[b] out of 0..capacity-1");
+  // one key chunk's partials must fit the static scratch
+  if (decode_partial_floats(n, num_seqs, n_heads, hd, 1) > KRAKEN_NOALLOC_SCRATCH_FLOATS)
+    return fail(KRAKEN_ERR_UNSUPPORTED,
+                "n * num_seqs * n_heads * (hd + 2) = " +
+                    std::to_string(decode_partial_floats(n, num_seqs, n_heads, hd, 1)) +
+                    " exceeds the static scratch of KRAKEN_NOALLOC_SCRATCH_FLOATS = " +
+                    std::to_string((int64_t)KRAKEN_NOALLOC_SCRATCH_FLOATS) + " floats");
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(KRAKEN_ERR_UNSUPPORTED, "device index");
+  float* part = nullptr;
+  {
+    // first call on this device (with the device current): look up its copy's address
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+      void* ptr = nullptr;
+      HIP_TRY(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+      if (!ptr) return fail(KRAKEN_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+      g_scratch_ptr[dev] = static_cast<float*>(ptr);
+    }
+    part = g_scratch_ptr[dev];
+  }
+  hipError_t e = launch_decode_attention((DType)dtype, qk, kv_layer, part,
+                                         KRAKEN_NOALLOC_SCRATCH_FLOATS, out, n, num_seqs, d,
+                                         n_heads, n_kv_heads, lens, max_seqs, capacity, 0,
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? KRAKEN_OK : hip_fail(e, "decode attention (static scratch)");
 }
 
 }  // extern "C"

@@ -22,6 +22,8 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OOM, ERR_STATE, ERR_HIP, ERR_OVERFLOW 
 DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 COMPUTE_CODES = {"storage": 0, "f32": 1, "bf16": 2, "f16": 3}
 MAX_SEQS = 256
+# floats of the static scratch of kraken_op_decode_attention_noalloc (kraken.h)
+NOALLOC_SCRATCH_FLOATS = 8 * 1024 * 1024
 
 # kernel classes of the per-kernel timer (kraken.h)
 K_LN1, K_GEMM_QK, K_GEMM_VT, K_ATTN, K_GEMM_O, K_COMBINE, K_GEMM_UP, K_GEMM_DOWN, K_CONCAT, \
@@ -91,6 +93,8 @@ def lib() -> ctypes.CDLL:
                                 i32),
         "kraken_op_decode_attention": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32), i32, i32,
                                         i32, vp, i64, vp], i32),
+        "kraken_op_decode_attention_noalloc": ([i32, vp, vp, vp, i32, i32, i32, i32, P(i32),
+                                                i32, i32, i32, vp], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(L, name)
@@ -444,3 +448,17 @@ def op_decode_attention(qk: torch.Tensor, kv_layer: torch.Tensor, out: torch.Ten
                                             n_kv_heads, arr, B, max_seqs, capacity,
                                             work.data_ptr(),
                                             work.numel(), _stream(stream)))
+
+
+def op_decode_attention_noalloc(qk: torch.Tensor, kv_layer: torch.Tensor, out: torch.Tensor,
+                                n: int, d: int, n_heads: int, lens: Sequence[int],
+                                max_seqs: int, capacity: int, stream=None,
+                                n_kv_heads: int = 0) -> None:
+    """op_decode_attention with the library's static scratch instead of a work buffer: the
+    call allocates nothing (kraken_op_decode_attention_noalloc)."""
+    B = len(lens)
+    arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
+    _check(lib().kraken_op_decode_attention_noalloc(dtype_code(qk.dtype), qk.data_ptr(),
+                                                    kv_layer.data_ptr(), out.data_ptr(), n, d,
+                                                    n_heads, n_kv_heads, arr, B, max_seqs,
+                                                    capacity, _stream(stream)))

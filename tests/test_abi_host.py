@@ -233,3 +233,9 @@ def test_binding_rejects_wrong_dtype_size_layout_and_device():
         args.update(kw)
         with pytest.raises(ValueError, match=pat):
             K().check_call_buffers(cfg, args["hidden"], 8, args["out"], args["sub_out"])
+
+
+def test_noalloc_scratch_size_matches_the_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define KRAKEN_NOALLOC_SCRATCH_FLOATS \((\d+) \* (\d+) \* (\d+)\)", text)
+    assert m and int(m[1]) * int(m[2]) * int(m[3]) == K().NOALLOC_SCRATCH_FLOATS
