@@ -17,9 +17,15 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                                           roofline of its dominant kernel)
        python bench.py --share G        (one GPU's part of a G-way split: N/G
                                           sub-layers per layer, no exchange)
+       python bench.py --engine MODEL --arch ARCH --ctx C
+                                        (the paper's TTFT engines, Section 4.3: the whole
+                                          model, tokens to the first token's logits, for
+                                          MODEL in 1.3b 6.7b 13b 65b 175b and ARCH in gpt
+                                          parallel kraken4 kraken8; one C-token prompt)
 """
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -92,13 +98,25 @@ def cpu_baseline(w, T, seed=0):
     O.sub_layer_forward(x, y, p, cu, w.n_heads, n_kv_heads=w.kv_heads)
     dt = time.perf_counter() - t0
     stack_s = dt * w.n_sub * w.n_layers
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = max([i.get("num_threads", 1) for i in blas] or [1])
     return {"value": T / stack_s, "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"1 of {w.n_sub} sub-layers x 1 of {w.n_layers} layers at the full "
                       f"{T}-token length ({dt:.1f} s, fp64 numpy), extrapolated x"
                       f"{w.n_sub * w.n_layers}",
+            "blas": [{"library": i.get("internal_api"), "version": i.get("version"),
+                      "threads": i.get("num_threads"), "arch": i.get("architecture")}
+                     for i in blas],
             "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def step_stats(per_step_ms):
+    """TTFT statistics over the timed steps (HIP event pairs around each step)."""
+    v = sorted(per_step_ms)
+    n = len(v)
+    return {"median": v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2]),
+            "min": v[0], "p90": v[min(n - 1, int(math.ceil(0.9 * n)) - 1)], "max": v[-1]}
 
 
 def traffic_of(kernel):
@@ -261,6 +279,65 @@ def bench_decode(args, w, compute):
     print(json.dumps(result), flush=True)
 
 
+def bench_engine(args):
+    """The whole model of one of the paper's TTFT engines (Section 4.3): token ids of one
+    prompt in, the first generated token's logits out (embeddings, every layer, W_concat
+    for Kraken, final LayerNorm, unembedding over 51,200 tokens), fp16, random weights."""
+    import torch
+
+    from paper_2408_07802_amd import kraken, synth
+
+    w = synth.engine_workload(args.engine, args.arch, args.ctx)
+    if args.layers:
+        w = dataclasses.replace(w, n_layers=args.layers, name=f"{w.name}-l{args.layers}")
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    cfg = kraken.Config(n_sub=w.n_sub, n_layers=w.n_layers, d_model=w.d_model,
+                        n_heads=w.n_heads, d_ff=w.d_ff, max_tokens=args.ctx, dtype=w.dtype,
+                        compute=w.compute, arch=w.arch, head_dim=w.head_size, vocab=w.vocab,
+                        max_positions=w.max_positions)
+    log(f"[bench engine] {w.name}: N={w.n_sub} L={w.n_layers} d={w.d_model} H={w.n_heads} "
+        f"hd={w.head_dim} F={w.d_ff} V={w.vocab}")
+    model = kraken.Kraken(cfg)
+    blob = kraken.pack_weights((synth.gen_layer(w, j, 0, dev) for j in range(w.n_layers)),
+                               synth.gen_w_concat(w, 0, dev) if w.arch == "kraken" else None,
+                               cfg, device=dev, embeddings=synth.gen_embeddings(w, 0, dev))
+    model.load_weights(blob)
+    torch.cuda.synchronize()
+    del blob
+    torch.cuda.empty_cache()
+    ids = synth.gen_tokens(w, args.ctx, 0)
+    cu = [0, args.ctx]
+    logits = torch.empty((1, w.vocab), dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        model.forward_tokens(ids, cu, logits=logits)
+    model.sync()
+    stream = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for k in range(args.steps):
+        model.forward_tokens(ids, cu, logits=logits)
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    model.sync()
+    per = [evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)]
+    flops = sum(kraken.class_flops(cfg, k, cu) for k in range(kraken.K_COUNT))
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    model.close()
+    print(json.dumps({
+        "metric": "TTFT ms (whole model, one prompt, 1 MI355X)", "value": ms, "unit": "ms",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "ttft_ms_stats": step_stats(per), "higher_is_better": False, "scaling": "strong",
+        "vs_baseline": None, "dtype": w.compute if w.compute != "storage" else w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "engine": args.engine, "arch": args.arch, "ctx": args.ctx,
+                   "n_sub": w.n_sub, "n_layers": w.n_layers, "d_model": w.d_model,
+                   "n_heads": w.n_heads, "head_dim": w.head_dim, "d_ff": w.d_ff,
+                   "vocab": w.vocab},
+        "mfma_util_pct": 100.0 * flops / (ms * 1e-3) / (MFMA_PEAK_TFLOPS["f16"] * 1e12),
+        "algorithmic_tflop_per_step": flops / 1e12}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -277,6 +354,12 @@ def main():
     ap.add_argument("--context", type=int, default=8192, help="decode: cached tokens each")
     ap.add_argument("--share", type=int, default=1,
                     help="run one GPU's share of a G-way split: N/G sub-layers per layer")
+    ap.add_argument("--engine", default=None, help="a TTFT engine of the paper's table")
+    ap.add_argument("--arch", default="kraken4", help="with --engine: gpt, parallel, kraken4, "
+                                                      "kraken8")
+    ap.add_argument("--ctx", type=int, default=2048, help="with --engine: prompt length")
+    ap.add_argument("--layers", type=int, default=0, help="with --engine: layer count "
+                                                          "(0: the engine's)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
@@ -285,7 +368,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import dataclasses
+    if args.engine:
+        bench_engine(args)
+        return
 
     import torch
 
@@ -339,18 +424,21 @@ def main():
         model.prefill(X, cu, out=out)
     torch.cuda.synchronize()
 
-    # ---- timed region: K steps, no instrumentation
+    # ---- timed region: K steps, no instrumentation (an event between steps: the per-step
+    # TTFT distribution; events on the prefill's stream cost nothing measurable)
     stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev0, ev1 = evs[0], evs[-1]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
+    for k in range(args.steps):
         model.prefill(X, cu, out=out)
-    ev1.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    ttft = step_stats([evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)])
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall / args.steps * 1e3:.3f})")
 
     # ---- per-kernel durations: the same K steps with HIP events around every launch
@@ -397,6 +485,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
         "ttft_ms": ms_per_step,
+        "ttft_ms_stats": ttft,
         "higher_is_better": True,
         "scaling": "strong",
         "vs_baseline": None,

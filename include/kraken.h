@@ -79,18 +79,28 @@ typedef enum {
   KRAKEN_COMPUTE_F16 = 3
 } kraken_compute;
 
+/* Layer architecture (Section 4.3 compares Kraken with the two others at equal sizes). */
+typedef enum {
+  KRAKEN_ARCH_KRAKEN = 0,    /* N sub-layers per layer, combine y, W_concat (Algorithm 1) */
+  KRAKEN_ARCH_GPT = 1,       /* standard pre-LN layer: h = x + MHA(LN1(x)), h + FFN(LN2(h)) */
+  KRAKEN_ARCH_PARALLEL = 2   /* parallel attention + FFN (GPT-J, PaLM): u = LN1(x),
+                                x + MHA(u) + FFN(u); its weight record has no ln2 */
+} kraken_arch;
+
 /*
  * Model shape (Section 3.1; heads are per sub-layer as in the paper's engine
  * table, Section 4.3).
- *   n_sub      N >= 1, parallel sub-layers per layer
+ *   n_sub      N >= 1, parallel sub-layers per layer (1 for the GPT-like and
+ *              parallel architectures)
  *   n_layers   L >= 1
- *   d_model    d, width of one sub-layer; multiple of 64
- *   n_heads    heads per sub-layer; d / n_heads must be 32, 64 or 128
- *   d_ff       MLP width; 0 means 4 d (Section 2.1); multiple of 64;
- *              d_ff * d * 4 < 2^31 and n_sub * d^2 * 4 < 2^31 (the repacked FFN and
- *              W_concat weights are addressed with 32-bit byte offsets)
+ *   d_model    d, width of one sub-layer; multiple of 4.  Widths that are not
+ *              multiples of 64 (the engine table's 1248, 3120, 5472, ...) are stored
+ *              padded to the next multiple of 64; results are those of width d.
+ *   n_heads    heads per sub-layer
+ *   d_ff       MLP width; 0 means 4 d (Section 2.1; the engine table's Kraken
+ *              models use 2 d, Section 3.2); multiple of 4
  *   max_tokens largest packed token count T a prefill may use (>= 1; at most
- *              4194304, and max_tokens * max(2 d, d_ff) * 4 < 2^31)
+ *              4194304, and max_tokens * (the widest stored activation row) * 4 < 2^31)
  *   dtype      a kraken_dtype: element type of the weight blob and of hidden_in
  *   compute    a kraken_compute: MFMA operand type (0 = same as dtype)
  *   ln_eps     LayerNorm epsilon; 0 means 1e-5
@@ -100,8 +110,24 @@ typedef enum {
  *              appendix on the KV cache size): the n_heads query heads form
  *              n_kv_heads groups of consecutive heads, and query head h reads
  *              key/value head h / (n_heads / n_kv_heads).  Must divide n_heads,
- *              and n_kv_heads * hd (the key and value width dkv) must be a
- *              multiple of 64.
+ *              and n_kv_heads * (stored head size) must be a multiple of 64.
+ *   arch       a kraken_arch (0 = Kraken)
+ *   head_dim   hd, the head size; 0 means d / n_heads (d must then be a multiple of
+ *              n_heads; Section 4.3: the width divided by the heads).  A multiple of 8
+ *              in 8..128; head sizes other than 32, 64 and 128 (the engine table's
+ *              72, 96, 104) are stored padded to the next of those, with the softmax
+ *              scale 1 / sqrt(hd) of the logical size.  The query width is
+ *              n_heads * hd (it may differ from d, as in GPT-3 13B: d = 5140, 40
+ *              heads of 128).
+ *   vocab      0: no embeddings (kraken_prefill takes the first-layer rows).  > 0:
+ *              token embedding rows, used again (tied) by the unembedding of
+ *              kraken_forward_tokens (Section 3.1: one set of embeddings, kept for
+ *              weight tying)
+ *   max_positions  position embedding rows (>= 1 when vocab > 0): the longest
+ *              sequence kraken_forward_tokens accepts
+ *   Weights: d_ff * d * 4, (query + key/value widths) * d * 4, n_sub * d^2 * 4
+ *   (Kraken) and vocab * d * 4 (stored widths) must stay below 2^31 (32-bit byte
+ *   offsets of the repacked weights).
  */
 typedef struct {
   int32_t n_sub;
@@ -114,6 +140,10 @@ typedef struct {
   int32_t compute;
   float ln_eps;
   int32_t n_kv_heads;
+  int32_t arch;
+  int32_t head_dim;
+  int32_t vocab;
+  int32_t max_positions;
 } kraken_config;
 
 typedef struct kraken_model kraken_model;
@@ -128,17 +158,20 @@ typedef struct kraken_model kraken_model;
  * Creates a model on the current device and allocates all device memory it
  * will use (weights and the activation workspace for max_tokens tokens).
  * The model owns that memory until kraken_destroy.  *out is set to NULL on
- * failure.  Errors: INVALID_ARG (null pointers, non-positive sizes),
- * UNSUPPORTED (d or d_ff not a multiple of 64, head size not 32/64/128,
+ * failure.  Errors: INVALID_ARG (null pointers, non-positive sizes, an unknown
+ * arch, n_sub != 1 for the GPT-like or parallel architecture), UNSUPPORTED (d or
+ * d_ff not a multiple of 4, a head size outside 8..128 or not a multiple of 8,
  * unknown dtype, sizes past the 32-bit offset limits above), OOM.
  */
 kraken_status kraken_create(const kraken_config* cfg, kraken_model** out);
 
 /*
- * Number of elements of the weight blob for cfg (0 for an invalid cfg), with
- * dkv = n_kv_heads * hd (= d for multi-head attention):
- *   L * N * (2 d^2 + 2 d dkv + 2 d F + 7 d + 2 dkv + F) + N d^2
- * (L * N * (4 d^2 + 2 d F + 9 d + F) + N d^2 when dkv = d).
+ * Number of elements of the weight blob for cfg (0 for an invalid cfg), with the
+ * logical query width dq = n_heads * hd and key/value width dkv = n_kv_heads * hd:
+ *   L * N * (2 d dq + 2 d dkv + 2 d F + 5 d + dq + 2 dkv + F + 2 d [no ln2 in
+ *   the parallel architecture]) + N d^2 [Kraken] + (vocab + max_positions) d + 2 d
+ *   [vocab > 0].  (The Kraken model with dq = dkv = d and no embeddings:
+ *   L * N * (4 d^2 + 2 d F + 9 d + F) + N d^2.)
  */
 size_t kraken_weight_blob_elems(const kraken_config* cfg);
 
@@ -147,10 +180,14 @@ size_t kraken_weight_blob_elems(const kraken_config* cfg);
  * logical order: for j in 0..L-1, for i in 0..N-1 (sub-layer i of layer j):
  *   ln1_g[d] ln1_b[d] Wqkv[d][d + 2 dkv] bqkv[d + 2 dkv] Wo[d][d] bo[d]
  *   ln2_g[d] ln2_b[d] W1[d][F] b1[F] W2[F][d] b2[d]
- * and then W_concat[N d][d].  Matrices are row-major and multiply as x W
- * ([in][out]); Wqkv's columns are [Q | K | V] (widths d, dkv, dkv), query
- * head h owns columns h*hd .. h*hd+hd-1 of Q and key/value head g columns
- * g*hd .. g*hd+hd-1 of K and of V; W_concat's row block i multiplies Y_i.
+ * and then W_concat[N d][d] (Kraken only), then, when vocab > 0,
+ *   tok_emb[vocab][d] pos_emb[max_positions][d] lnf_g[d] lnf_b[d].
+ * The GPT-like and parallel architectures have one record per layer (N = 1);
+ * the parallel record omits ln2_g and ln2_b.  Matrices are row-major and
+ * multiply as x W ([in][out]); Wqkv is [d][dq + 2 dkv] with columns [Q | K | V],
+ * query head h owns columns h*hd .. h*hd+hd-1 of Q and key/value head g columns
+ * g*hd .. g*hd+hd-1 of K and of V; Wo is [dq][d]; W_concat's row block i
+ * multiplies Y_i.
  * blob_is_device selects whether `blob` is device or host memory.  The call
  * copies and repacks the blob into the model's own layout; the caller keeps
  * ownership and may free or reuse the blob once the stream has synchronised.
@@ -185,6 +222,29 @@ kraken_status kraken_load_weights(kraken_model* m, const void* blob, size_t nbyt
  */
 kraken_status kraken_prefill(kraken_model* m, const void* hidden_in, const int32_t* cu_seqlens,
                              int32_t num_seqs, float* hidden_out, float* sub_out, void* stream);
+
+/*
+ * The whole model on packed token sequences (Section 2.1: embeddings, the layer
+ * stack, the unembedding; Section 3.1: one token and position embedding shared by
+ * the first layer's sub-layers, W_concat's output feeds the unembedding).  Needs a
+ * model with vocab > 0.
+ *   token_ids   HOST int32[T], each in 0 .. vocab-1; T = cu_seqlens[num_seqs].
+ *   cu_seqlens  HOST, as for kraken_prefill; every sequence at most max_positions
+ *               long.  Token t of sequence b has position t - cu[b].
+ *   logits      device float32 [num_seqs][vocab]: the next-token logits of each
+ *               sequence's last token, LN_f(h) tok_emb^T (the unembedding tied to
+ *               the token embedding, after a final LayerNorm), where h is the
+ *               stack's output row (W_concat's, for Kraken).
+ *   hidden_out  NULL or device float32 [T][d]: h for every token.
+ * The ids are copied through a pinned host buffer the model owns; the call returns
+ * once the copy is enqueued (a following call waits for it before reusing the
+ * buffer).  Errors: INVALID_ARG (an id out of range, a sequence longer than
+ * max_positions, overlapping outputs, bad cu_seqlens), STATE (no embeddings, weights
+ * not loaded), HIP.  Activation overflow of fp16 operands: see kraken_sync.
+ */
+kraken_status kraken_forward_tokens(kraken_model* m, const int32_t* token_ids,
+                                    const int32_t* cu_seqlens, int32_t num_seqs, float* logits,
+                                    float* hidden_out, void* stream);
 
 /* ------------------------------------------------------------------------
  * KV cache and one-token decode (Section 2.1, KV cache: the keys and values
@@ -275,13 +335,14 @@ enum {
   KRAKEN_K_GEMM_VT = 2,    /* V projection (written transposed) */
   KRAKEN_K_ATTN = 3,       /* causal flash attention */
   KRAKEN_K_GEMM_O = 4,     /* output projection + residual */
-  KRAKEN_K_COMBINE = 5,    /* N-way sum + residual + LayerNorm before FFN */
+  KRAKEN_K_COMBINE = 5,    /* N-way sum + residual + LayerNorm before FFN (GPT-like: LN2) */
   KRAKEN_K_GEMM_UP = 6,    /* FFN up projection + GELU */
   KRAKEN_K_GEMM_DOWN = 7,  /* FFN down projection + residual */
   KRAKEN_K_CONCAT = 8,     /* W_concat (and its operand split) */
-  KRAKEN_K_OTHER = 9,      /* input conversion, output copies */
+  KRAKEN_K_OTHER = 9,      /* input conversion, output copies, embedding, final LayerNorm */
   KRAKEN_K_KV = 10,        /* KV cache writes (kraken_prefill_kv, kraken_decode) */
-  KRAKEN_K_COUNT = 11
+  KRAKEN_K_UNEMBED = 11,   /* unembedding GEMM (kraken_forward_tokens) */
+  KRAKEN_K_COUNT = 12
 };
 kraken_status kraken_profile_enable(kraken_model* m, int enable);
 kraken_status kraken_profile_read(kraken_model* m, int kernel_class, double* total_ms,

@@ -371,6 +371,28 @@ def parallel_block_forward(x, p: Mapping, cu_seqlens, n_heads: int, eps: float =
         feed_forward(u, p)
 
 
+def stack_forward(X, cu_seqlens: Sequence[int], arch: str,
+                  layers: Iterable[Sequence[Mapping]], n_heads: int, W_concat=None,
+                  eps: float = LN_EPS, head_dim: int | None = None,
+                  n_kv_heads: int | None = None) -> np.ndarray:
+    """The layer stack on first-layer rows ``X``: for "kraken" the Kraken layers and
+    W_concat (``kraken_prefill``'s ``out``); for "gpt" / "parallel" the standard or the
+    parallel layers (one parameter mapping per layer) in sequence, returning the last
+    layer's output."""
+    if arch not in ARCHS:
+        raise ValueError(f"unknown architecture {arch!r}")
+    if arch == "kraken":
+        out, _ = kraken_prefill(X, cu_seqlens, layers, W_concat, n_heads, eps,
+                                n_kv_heads=n_kv_heads, head_dim=head_dim)
+        return out
+    block = gpt_block_forward if arch == "gpt" else parallel_block_forward
+    hidden = _f64(X)
+    for layer in layers:
+        (p,) = layer
+        hidden = block(hidden, p, cu_seqlens, n_heads, eps, head_dim)
+    return hidden
+
+
 def unembed(h, lnf_g, lnf_b, tok_emb, eps: float = LN_EPS) -> np.ndarray:
     """Next-token logits of the rows of ``h``: ``LN_f(h) @ tok_emb^T`` (tied weights)."""
     return layer_norm(h, lnf_g, lnf_b, eps) @ _f64(tok_emb).T
@@ -389,18 +411,9 @@ def model_forward(token_ids, cu_seqlens: Sequence[int], arch: str,
     last token of every sequence (the first generated token's distribution, what the
     time to first token measures) and the unembedding's input ``hidden [T, d]``.
     """
-    if arch not in ARCHS:
-        raise ValueError(f"unknown architecture {arch!r}")
     X = embed(token_ids, cu_seqlens, emb["tok_emb"], emb["pos_emb"])
-    if arch == "kraken":
-        hidden, _ = kraken_prefill(X, cu_seqlens, layers, W_concat, n_heads, eps,
-                                   n_kv_heads=n_kv_heads, head_dim=head_dim)
-    else:
-        block = gpt_block_forward if arch == "gpt" else parallel_block_forward
-        hidden = X
-        for layer in layers:
-            (p,) = layer
-            hidden = block(hidden, p, cu_seqlens, n_heads, eps, head_dim)
+    hidden = stack_forward(X, cu_seqlens, arch, layers, n_heads, W_concat, eps, head_dim,
+                           n_kv_heads)
     last = [int(c) - 1 for c in cu_seqlens[1:]]
     return unembed(hidden[last], emb["lnf_g"], emb["lnf_b"], emb["tok_emb"], eps), hidden
 

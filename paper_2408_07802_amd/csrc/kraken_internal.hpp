@@ -104,16 +104,37 @@ inline int vt_ld(int T) { return (T + 63) & ~63; }
 hipError_t launch_zero_cols(DType dt, void* base, int64_t rows, int64_t ld, int c0, int c1,
                             hipStream_t s);
 
-// LayerNorm of n rows-sets: out[i][t] = LN(x[i*xs + t*d]) with per-i gamma/beta.
+// LayerNorm of n rows-sets: out[i][t] = LN(x[i*xs + t*d]) with per-i gamma/beta.  Rows are
+// d wide (the stored width); the statistics cover the first dl (logical width, a multiple
+// of 4; padding columns past it hold zeros and have gamma = beta = 0).
 // ovf (fp16 outputs; may be NULL): set to 1 when an output overflows the fp16 range.
 hipError_t launch_layernorm(DType dt, const float* x, int64_t x_batch_stride, const float* gamma,
-                            const float* beta, void* out, int n, int T, int d, float eps,
+                            const float* beta, void* out, int n, int T, int d, int dl, float eps,
                             int* ovf, hipStream_t s);
 
-// out[i][t] = LN(h[i][t] + y[t]); y = shared[t] or sum_k x[k][t].  ovf as for LN1.
+// out[i][t] = LN(h[i][t] + y[t]); y = shared[t] or sum_k x[k][t].  d, dl, ovf as for LN1.
 hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
                               const float* gamma, const float* beta, void* out, int n, int T,
-                              int d, float eps, int* ovf, hipStream_t s);
+                              int d, int dl, float eps, int* ovf, hipStream_t s);
+
+// dst[r * dst_ld + pad(c)] = float(src[r * src_ld + c]) for r < R, c < C, with
+// pad(c) = (c / g) * gp + c % g (logical element c of group c / g, placed in a group of gp
+// slots; g = gp: no padding).  Untouched destination elements keep their values.
+hipError_t launch_to_f32_2d(DType st, const void* src, int64_t src_ld, float* dst,
+                            int64_t dst_ld, int R, int C, int g, int gp, hipStream_t s);
+
+// dst[r * dst_ld + c] = Dst(src[r * src_ld + c]) for r < R, c < C; *overflow as for
+// launch_transpose.
+hipError_t launch_convert_2d(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
+                             int64_t dst_ld, int R, int C, int* overflow, hipStream_t s);
+
+// X[t][c] = tok[ids[t]][c] + pos[pos_ids[t]][c] for c < dp (device ids and positions).
+hipError_t launch_embed(DType dt, const int* ids, const int* pos_ids, const void* tok,
+                        const float* pos, float* X, int T, int dp, hipStream_t s);
+
+// dst[b][:] = src[rows[b]][:], fp32 rows of dp elements (device rows).
+hipError_t launch_gather_rows(const float* src, const int* rows, float* dst, int B, int dp,
+                              hipStream_t s);
 
 // dst[k] = float(src[k]) for k < count.
 hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, hipStream_t s);
@@ -123,10 +144,13 @@ hipError_t launch_to_f32(DType dt, const void* src, float* dst, int64_t count, h
 hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, int* ovf,
                           hipStream_t s);
 
-// dst[c][r] = Dst(src[r*src_ld + c]) for r < R, c < C, dst row stride dst_ld.  When the
-// destination is fp16 and a finite source value does not fit, *overflow is set to 1.
+// dst[pad_c(c)][pad_r(r)] = Dst(src[r*src_ld + c]) for r < R, c < C, dst row stride dst_ld,
+// with pad_r(r) = (r / gr) * grp + r % gr and pad_c likewise with (gc, gcp) (see
+// launch_to_f32_2d; gr = grp and gc = gcp: a plain transpose).  When the destination is
+// fp16 and a finite source value does not fit, *overflow is set to 1.
 hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
-                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s);
+                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s,
+                            int gr = 1, int grp = 1, int gc = 1, int gcp = 1);
 
 // KV cache of one layer: [n][2 (K, V)][max_seqs][n_kv_heads][capacity][hd], compute
 // type; dkv = n_kv_heads * hd.  Prefill: K from columns d .. d+dkv-1 of qk [n][T][d + dkv],

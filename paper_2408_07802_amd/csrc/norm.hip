@@ -94,22 +94,26 @@ __device__ __forceinline__ void flag_overflow(float amax, int* ovf) {
   }
 }
 
+// Statistics of a row over its first dl (logical) elements, dl a multiple of 4: a row
+// stored with padding columns past dl (a width rounded up for the kernels) keeps them out
+// of the mean and the variance.
 template <int V>
-__device__ __forceinline__ void row_stats(const float4* v, int nv, int d, float eps,
+__device__ __forceinline__ void row_stats(const float4* v, int nv, int dl, float eps,
                                           float* red, float& mean, float& rstd) {
   float s = 0.f;
 #pragma unroll
   for (int u = 0; u < V; ++u)
-    if (u < nv) s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
-  mean = block_sum(s, red) / (float)d;
+    if (u < nv && (threadIdx.x + u * NORM_THREADS) * 4 < dl)
+      s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+  mean = block_sum(s, red) / (float)dl;
   float q = 0.f;
 #pragma unroll
   for (int u = 0; u < V; ++u)
-    if (u < nv) {
+    if (u < nv && (threadIdx.x + u * NORM_THREADS) * 4 < dl) {
       const float a = v[u].x - mean, b = v[u].y - mean, c = v[u].z - mean, e = v[u].w - mean;
       q += (a * a + b * b) + (c * c + e * e);
     }
-  const float var = block_sum(q, red) / (float)d;
+  const float var = block_sum(q, red) / (float)dl;
   rstd = rsqrtf(var + eps);
 }
 
@@ -131,7 +135,7 @@ __device__ __forceinline__ int my_vecs(int d) {
 template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
     const float* __restrict__ x, int64_t xs, const float* __restrict__ gamma,
-    const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, float eps,
+    const float* __restrict__ beta, S* __restrict__ out, int n, int T, int d, int dl, float eps,
     int* __restrict__ ovf) {
   __shared__ float red[NORM_THREADS / 64];
   const int t = blockIdx.x;
@@ -148,7 +152,7 @@ __global__ __launch_bounds__(NORM_THREADS) void layernorm_kernel(
 #pragma unroll
       for (int u = 0; u < V; ++u)
         if (u < nv) v[u] = *reinterpret_cast<const float4*>(row + (threadIdx.x + u * NORM_THREADS) * 4);
-      row_stats<V>(v, nv, d, eps, red, mean, rstd);
+      row_stats<V>(v, nv, dl, eps, red, mean, rstd);
     }
     amax = fmaxf(amax, ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d,
                                       beta + (int64_t)i * d, out + ((int64_t)i * T + t) * d));
@@ -160,7 +164,7 @@ template <typename S, int V>
 __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
     const float* __restrict__ x, const float* __restrict__ shared, const float* __restrict__ h,
     const float* __restrict__ gamma, const float* __restrict__ beta, S* __restrict__ out, int n,
-    int T, int d, float eps, int* __restrict__ ovf) {
+    int T, int d, int dl, float eps, int* __restrict__ ovf) {
   __shared__ float red[NORM_THREADS / 64];
   float amax = 0.f;
   const int t = blockIdx.x;
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(NORM_THREADS) void combine_ln2_kernel(
       v[u] = make_float4(a.x + y[u].x, a.y + y[u].y, a.z + y[u].z, a.w + y[u].w);
     }
     float mean, rstd;
-    row_stats<V>(v, nv, d, eps, red, mean, rstd);
+    row_stats<V>(v, nv, dl, eps, red, mean, rstd);
     amax = fmaxf(amax, ln_write<S, V>(v, nv, mean, rstd, gamma + (int64_t)i * d,
                                       beta + (int64_t)i * d, out + (i * plane + (int64_t)t * d)));
   }
@@ -231,10 +235,17 @@ __global__ void split16_kernel(const float* __restrict__ src, S* __restrict__ ds
   flag_overflow<S>(amax, ovf);
 }
 
+// Index of logical element x in a padded layout: x's group of g elements (a head of hd
+// features, or a sub-layer's d features) starts at (x / g) * gp.  g = gp: the identity.
+__device__ __forceinline__ int64_t pad_index(int64_t x, int g, int gp) {
+  return g == gp ? x : (x / g) * gp + x % g;
+}
+
 template <typename Src, typename Dst>
 __global__ __launch_bounds__(256) void transpose_kernel(const Src* __restrict__ src, int64_t sld,
                                                         Dst* __restrict__ dst, int64_t dld, int R,
-                                                        int C, int* __restrict__ overflow) {
+                                                        int C, int* __restrict__ overflow,
+                                                        int gr, int grp, int gc, int gcp) {
   __shared__ float tile[64][65];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -250,10 +261,67 @@ __global__ __launch_bounds__(256) void transpose_kernel(const Src* __restrict__ 
       const float v = tile[tx][k];
       const Dst o = (Dst)v;
       if constexpr (__is_same(Dst, f16)) over |= (__builtin_isinf((float)o) && !__builtin_isinf(v));
-      dst[(int64_t)c * dld + r] = o;
+      dst[pad_index(c, gc, gcp) * dld + pad_index(r, gr, grp)] = o;
     }
   }
   if (over && overflow) *overflow = 1;
+}
+
+// dst[r * dld + pad_index(c)] = float(src[r * sld + c]) for r < R, c < C.
+template <typename S>
+__global__ void to_f32_2d_kernel(const S* __restrict__ src, int64_t sld, float* __restrict__ dst,
+                                 int64_t dld, int R, int C, int g, int gp) {
+  const int64_t total = (int64_t)R * C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += stride) {
+    const int64_t r = k / C, c = k % C;
+    dst[r * dld + pad_index(c, g, gp)] = (float)src[r * sld + c];
+  }
+}
+
+// dst[r * dld + c] = Dst(src[r * sld + c]) for r < R, c < C (rows converted in place, no
+// transpose); a finite value that overflows an fp16 destination sets *overflow.
+template <typename Src, typename Dst>
+__global__ void convert_2d_kernel(const Src* __restrict__ src, int64_t sld, Dst* __restrict__ dst,
+                                  int64_t dld, int R, int C, int* __restrict__ overflow) {
+  const int64_t total = (int64_t)R * C;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  bool over = false;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += stride) {
+    const int64_t r = k / C, c = k % C;
+    const float v = (float)src[r * sld + c];
+    const Dst o = (Dst)v;
+    if constexpr (__is_same(Dst, f16)) over |= (__builtin_isinf((float)o) && !__builtin_isinf(v));
+    dst[r * dld + c] = o;
+  }
+  if (over && overflow) *overflow = 1;
+}
+
+// First-layer input of a token sequence: X[t] = tok[ids[t]] + pos[pos_ids[t]] over the
+// (padded) row width dp.  Token rows in the MFMA operand type (the table the tied
+// unembedding multiplies), position rows in fp32.  ids[] were checked against the table
+// size on the host.
+template <typename S>
+__global__ __launch_bounds__(256) void embed_kernel(const int* __restrict__ ids,
+                                                    const int* __restrict__ pos_ids,
+                                                    const S* __restrict__ tok,
+                                                    const float* __restrict__ pos,
+                                                    float* __restrict__ X, int dp) {
+  const int t = blockIdx.x;
+  const S* trow = tok + (int64_t)ids[t] * dp;
+  const float* prow = pos + (int64_t)pos_ids[t] * dp;
+  float* xrow = X + (int64_t)t * dp;
+  for (int c = threadIdx.x; c < dp; c += 256) xrow[c] = (float)trow[c] + prow[c];
+}
+
+// dst[b] = src[rows[b]] (fp32 rows of width dp).
+__global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restrict__ src,
+                                                          const int* __restrict__ rows,
+                                                          float* __restrict__ dst, int dp) {
+  const int b = blockIdx.x;
+  const float4* srow = reinterpret_cast<const float4*>(src + (int64_t)rows[b] * dp);
+  float4* drow = reinterpret_cast<float4*>(dst + (int64_t)b * dp);
+  for (int c = threadIdx.x; c < dp / 4; c += 256) drow[c] = srow[c];
 }
 
 template <typename S>
@@ -292,10 +360,11 @@ unsigned sub_groups(int n, int T) {
 }  // namespace
 
 hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* gamma,
-                            const float* beta, void* out, int n, int T, int d, float eps,
+                            const float* beta, void* out, int n, int T, int d, int dl, float eps,
                             int* ovf, hipStream_t s) {
   if (T <= 0 || n <= 0) return hipSuccess;
-  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
+  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4 || dl % 4 != 0 || dl < 4 || dl > d)
+    return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
     // one workgroup per (token, sub-layer) row when the rows differ (more rows in flight);
@@ -303,10 +372,10 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
     const dim3 grid(T, xs != 0 ? (unsigned)n : sub_groups(n, T)), block(NORM_THREADS);
     S* o = static_cast<S*>(out);
     switch (vecs_for(d)) {
-      case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
-      case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
-      case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
-      default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
     }
     return hipGetLastError();
   });
@@ -314,18 +383,19 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
 
 hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, const float* h,
                               const float* gamma, const float* beta, void* out, int n, int T,
-                              int d, float eps, int* ovf, hipStream_t s) {
+                              int d, int dl, float eps, int* ovf, hipStream_t s) {
   if (T <= 0 || n <= 0) return hipSuccess;
-  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4) return hipErrorInvalidValue;
+  if (d % 4 != 0 || d > NORM_THREADS * MAX_VEC * 4 || dl % 4 != 0 || dl < 4 || dl > d)
+    return hipErrorInvalidValue;
   return by_type(dt, [&](auto tag) {
     using S = decltype(tag);
     const dim3 grid(T, sub_groups(n, T)), block(NORM_THREADS);
     S* o = static_cast<S*>(out);
     switch (vecs_for(d)) {
-      case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
-      case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
-      case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
-      default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, eps, ovf); break;
+      case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
     }
     return hipGetLastError();
   });
@@ -378,8 +448,10 @@ hipError_t launch_split16(DType dt, const float* src, void* dst, int64_t count, 
 }
 
 hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
-                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s) {
+                            int64_t dst_ld, int R, int C, int* overflow, hipStream_t s,
+                            int gr, int grp, int gc, int gcp) {
   if (R <= 0 || C <= 0) return hipSuccess;
+  if (gr < 1 || grp < gr || gc < 1 || gcp < gc) return hipErrorInvalidValue;
   dim3 grid((C + 63) / 64, (R + 63) / 64), block(256);
   return by_type(src_t, [&](auto stag) {
     using Src = decltype(stag);
@@ -387,7 +459,53 @@ hipError_t launch_transpose(DType src_t, const void* src, int64_t src_ld, DType 
       using Dst = decltype(dtag);
       hipLaunchKernelGGL((transpose_kernel<Src, Dst>), grid, block, 0, s,
                          static_cast<const Src*>(src), src_ld, static_cast<Dst*>(dst), dst_ld, R,
-                         C, overflow);
+                         C, overflow, gr, grp, gc, gcp);
+      return hipGetLastError();
+    });
+  });
+}
+
+hipError_t launch_to_f32_2d(DType st, const void* src, int64_t src_ld, float* dst,
+                            int64_t dst_ld, int R, int C, int g, int gp, hipStream_t s) {
+  if (R <= 0 || C <= 0) return hipSuccess;
+  if (g < 1 || gp < g) return hipErrorInvalidValue;
+  return by_type(st, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(to_f32_2d_kernel<S>, dim3(grid_for((int64_t)R * C)), dim3(256), 0, s,
+                       static_cast<const S*>(src), src_ld, dst, dst_ld, R, C, g, gp);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_embed(DType dt, const int* ids, const int* pos_ids, const void* tok,
+                        const float* pos, float* X, int T, int dp, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  return by_type(dt, [&](auto tag) {
+    using S = decltype(tag);
+    hipLaunchKernelGGL(embed_kernel<S>, dim3(T), dim3(256), 0, s, ids, pos_ids,
+                       static_cast<const S*>(tok), pos, X, dp);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_gather_rows(const float* src, const int* rows, float* dst, int B, int dp,
+                              hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (dp % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(B), dim3(256), 0, s, src, rows, dst, dp);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_2d(DType src_t, const void* src, int64_t src_ld, DType dst_t, void* dst,
+                             int64_t dst_ld, int R, int C, int* overflow, hipStream_t s) {
+  if (R <= 0 || C <= 0) return hipSuccess;
+  return by_type(src_t, [&](auto stag) {
+    using Src = decltype(stag);
+    return by_type(dst_t, [&](auto dtag) {
+      using Dst = decltype(dtag);
+      hipLaunchKernelGGL((convert_2d_kernel<Src, Dst>), dim3(grid_for((int64_t)R * C)), dim3(256),
+                         0, s, static_cast<const Src*>(src), src_ld, static_cast<Dst*>(dst),
+                         dst_ld, R, C, overflow);
       return hipGetLastError();
     });
   });

@@ -25,18 +25,22 @@ MAX_SEQS = 256
 # floats of the static scratch of kraken_op_decode_attention_noalloc (kraken.h)
 NOALLOC_SCRATCH_FLOATS = 8 * 1024 * 1024
 
+ARCH_CODES = {"kraken": 0, "gpt": 1, "parallel": 2}
+
 # kernel classes of the per-kernel timer (kraken.h)
 K_LN1, K_GEMM_QK, K_GEMM_VT, K_ATTN, K_GEMM_O, K_COMBINE, K_GEMM_UP, K_GEMM_DOWN, K_CONCAT, \
-    K_OTHER, K_KV = range(11)
-K_COUNT = 11
+    K_OTHER, K_KV, K_UNEMBED = range(12)
+K_COUNT = 12
 KERNEL_CLASS_NAMES = ["ln1", "gemm_qk", "gemm_vt", "attention", "gemm_o", "combine_ln2",
-                      "gemm_up", "gemm_down", "w_concat", "other", "kv_cache"]
+                      "gemm_up", "gemm_down", "w_concat", "other", "kv_cache", "unembed"]
 
 EPI_BIAS_N, EPI_BIAS_N_GELU, EPI_BIAS_N_RES, EPI_BIAS_M = range(4)
 
-# Order of one sub-layer's tensors in the weight blob (kraken_load_weights).
+# Order of one sub-layer's tensors in the weight blob (kraken_load_weights); the parallel
+# attention + FFN layer has no ln2_g / ln2_b.  Embeddings follow the layers (and W_concat).
 BLOB_ORDER = ("ln1_g", "ln1_b", "Wqkv", "bqkv", "Wo", "bo",
               "ln2_g", "ln2_b", "W1", "b1", "W2", "b2")
+EMB_ORDER = ("tok_emb", "pos_emb", "lnf_g", "lnf_b")
 
 
 class KrakenError(RuntimeError):
@@ -50,7 +54,9 @@ class _Config(ctypes.Structure):
                 ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("d_ff", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float), ("n_kv_heads", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("n_kv_heads", ctypes.c_int32),
+                ("arch", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("max_positions", ctypes.c_int32)]
 
 
 _lib = None
@@ -73,6 +79,7 @@ def lib() -> ctypes.CDLL:
         "kraken_weight_blob_elems": ([P(_Config)], sz),
         "kraken_load_weights": ([vp, vp, sz, ctypes.c_int, vp], i32),
         "kraken_prefill": ([vp, vp, P(i32), i32, vp, vp, vp], i32),
+        "kraken_forward_tokens": ([vp, P(i32), P(i32), i32, vp, vp, vp], i32),
         "kraken_kv_cache_bytes": ([P(_Config), i32, i32], sz),
         "kraken_prefill_kv": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
         "kraken_decode": ([vp, vp, P(i32), i32, vp, vp, vp, i32, i32, vp], i32),
@@ -190,15 +197,29 @@ class Config:
     compute: str = "storage"     # MFMA operand type: "storage", "f32", "bf16" or "f16"
     ln_eps: float = 0.0
     n_kv_heads: int = 0          # key/value heads (0: n_heads; fewer: grouped-query)
+    arch: str = "kraken"         # "kraken", "gpt" (standard layer) or "parallel"
+    head_dim: int = 0            # 0: d_model / n_heads
+    vocab: int = 0               # token embedding rows (0: no embeddings)
+    max_positions: int = 0       # position embedding rows
 
     @property
     def kv_heads(self) -> int:
         return self.n_kv_heads or self.n_heads
 
+    @property
+    def hd(self) -> int:
+        return self.head_dim or self.d_model // self.n_heads
+
+    @property
+    def stored_head_dim(self) -> int:
+        """Head size as stored (32, 64 or 128): the KV cache's row length."""
+        return 32 if self.hd <= 32 else 64 if self.hd <= 64 else 128
+
     def c_struct(self) -> _Config:
         return _Config(self.n_sub, self.n_layers, self.d_model, self.n_heads, self.d_ff,
                        self.max_tokens, dtype_code(self.dtype), COMPUTE_CODES[self.compute],
-                       self.ln_eps, self.n_kv_heads)
+                       self.ln_eps, self.n_kv_heads, ARCH_CODES[self.arch], self.head_dim,
+                       self.vocab, self.max_positions)
 
 
 def weight_blob_elems(cfg: Config) -> int:
@@ -213,21 +234,35 @@ def class_flops(cfg: Config, kernel_class: int, cu: Sequence[int]) -> float:
 
 
 def pack_weights(layers: Iterable[Sequence[Mapping[str, torch.Tensor]]],
-                 w_concat: torch.Tensor, cfg: Config, device=None) -> torch.Tensor:
-    """Flattens per-(layer, sub-layer) tensors into the blob order of kraken_load_weights."""
+                 w_concat: Optional[torch.Tensor], cfg: Config, device=None,
+                 embeddings: Optional[Mapping[str, torch.Tensor]] = None) -> torch.Tensor:
+    """Flattens per-(layer, sub-layer) tensors into the blob order of kraken_load_weights:
+    the layers, W_concat (Kraken only; None otherwise), then the embeddings (tok_emb,
+    pos_emb, lnf_g, lnf_b) when the model has a vocabulary."""
     dt = torch_dtype(dtype_code(cfg.dtype))
-    device = device if device is not None else w_concat.device
+    if device is None:
+        device = w_concat.device if w_concat is not None else "cuda"
     blob = torch.empty(weight_blob_elems(cfg), dtype=dt, device=device)
+    names = [n for n in BLOB_ORDER if cfg.arch != "parallel" or n not in ("ln2_g", "ln2_b")]
     off = 0
+
+    def put(t):
+        nonlocal off
+        t = t.reshape(-1)
+        blob[off:off + t.numel()].copy_(t)
+        off += t.numel()
+
     for layer in layers:
         for sub in layer:
-            for name in BLOB_ORDER:
-                t = sub[name].reshape(-1)
-                blob[off:off + t.numel()].copy_(t)
-                off += t.numel()
-    t = w_concat.reshape(-1)
-    blob[off:off + t.numel()].copy_(t)
-    off += t.numel()
+            for name in names:
+                put(sub[name])
+    if cfg.arch == "kraken":
+        put(w_concat)
+    elif w_concat is not None:
+        raise ValueError("only the Kraken architecture has W_concat")
+    if cfg.vocab:
+        for name in EMB_ORDER:
+            put(embeddings[name])
     if off != blob.numel():
         raise ValueError(f"blob has {off} elements, expected {blob.numel()}")
     return blob
@@ -243,7 +278,7 @@ class KVCache:
 
     def view(self, cfg: "Config") -> torch.Tensor:
         """The cache as a tensor [L, N, 2, max_seqs, kv_heads, capacity, hd]."""
-        hd = cfg.d_model // cfg.n_heads
+        hd = cfg.stored_head_dim
         dt = torch_dtype(compute_code(cfg))
         return self.buf.view(dt).view(cfg.n_layers, cfg.n_sub, 2, self.max_seqs, cfg.kv_heads,
                                       self.capacity, hd)
@@ -296,6 +331,34 @@ class Kraken:
         _check(lib().kraken_prefill(self._h, hidden.data_ptr(), cu, len(cu_seqlens) - 1,
                                     out.data_ptr(), _ptr(sub_out), _stream(stream)))
         return out, sub_out
+
+    def forward_tokens(self, token_ids: Sequence[int], cu_seqlens: Sequence[int],
+                       logits: Optional[torch.Tensor] = None, hidden_out=False, device=None,
+                       stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+        """The whole model on packed token sequences: returns (logits [num_seqs, vocab] of
+        each sequence's last token, hidden [T, d] (the unembedding's input) or None)."""
+        import numpy as np
+        ids = np.ascontiguousarray(np.asarray(token_ids, dtype=np.int32))
+        T, B, V = int(cu_seqlens[-1]), len(cu_seqlens) - 1, self.cfg.vocab
+        if ids.shape != (T,):
+            raise ValueError(f"token_ids has shape {ids.shape}, expected ({T},)")
+        device = device or "cuda"
+        if logits is None:
+            logits = torch.empty((B, V), dtype=torch.float32, device=device)
+        check_device_tensor("logits", logits, torch.float32, B * V)
+        if hidden_out is True:
+            hidden_out = torch.empty((T, self.cfg.d_model), dtype=torch.float32,
+                                     device=logits.device)
+        elif hidden_out is False:
+            hidden_out = None
+        if hidden_out is not None:
+            check_device_tensor("hidden_out", hidden_out, torch.float32, T * self.cfg.d_model,
+                                logits.device)
+        cu = _cu_array(cu_seqlens)
+        _check(lib().kraken_forward_tokens(
+            self._h, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cu, B,
+            logits.data_ptr(), _ptr(hidden_out), _stream(stream)))
+        return logits, hidden_out
 
     # ---- KV cache and decode
     def kv_cache_bytes(self, max_seqs: int, capacity: int) -> int:

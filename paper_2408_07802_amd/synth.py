@@ -34,7 +34,8 @@ import torch
 
 __all__ = ["Workload", "WORKLOADS", "workload", "seq_lens", "cu_seqlens",
            "gen_hidden", "gen_sub_layer", "gen_layer", "gen_w_concat", "torch_dtype",
-           "compute_dtype", "gen_cached_kv"]
+           "compute_dtype", "gen_cached_kv", "ENGINES", "engine_workload", "gen_tokens",
+           "gen_embeddings"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -52,10 +53,14 @@ class Workload:
     out_proj_std: Optional[float] = None       # std of Wo and W2 (None: w_std)
     compute: str = "storage"                   # MFMA operand type the prefill runs with
     n_kv_heads: int = 0                        # key/value heads (0: n_heads)
+    arch: str = "kraken"                       # "kraken", "gpt" or "parallel"
+    head_size: int = 0                         # 0: d_model / n_heads
+    vocab: int = 0                             # token embedding rows (0: no embeddings)
+    max_positions: int = 0                     # position embedding rows
 
     @property
     def head_dim(self) -> int:
-        return self.d_model // self.n_heads
+        return self.head_size or self.d_model // self.n_heads
 
     @property
     def kv_heads(self) -> int:
@@ -96,9 +101,46 @@ WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
 # one causal sequence of 8192 tokens.
 BENCH_WORKLOAD = "kraken-n8-l24-d2048-h16-s8192-bf16"
 
+# The paper's TTFT engines (Section 4.3, table of engine configurations): layers, the
+# GPT-like width and heads (shared by the parallel attention + FFN engine), and the 4-way
+# and 8-way Kraken widths and heads per sub-layer.  The GPT-like engines have an FFN of 4d,
+# the Kraken engines of 2d (Section 3.2).  The 65B and 175B engines were built with a
+# quarter of the layers; the 13B GPT-like width 5140 with 40 heads has heads of 128 (the
+# GPT-3 13B configuration; 5140 / 40 is not an integer).  Vocabulary 51,200 and prompts of
+# up to 2048 tokens (Section 4.3).
+ENGINES = {
+    "1.3b": dict(layers=24, gpt=(2048, 16), kraken4=(1248, 12), kraken8=(960, 10)),
+    "6.7b": dict(layers=32, gpt=(4096, 32), kraken4=(2496, 24), kraken8=(1920, 20)),
+    "13b": dict(layers=40, gpt=(5140, 40), kraken4=(3120, 30), kraken8=(2304, 32),
+                gpt_head=128),
+    "65b": dict(layers=20, gpt=(8192, 64), kraken4=(4992, 39), kraken8=(3648, 38)),
+    "175b": dict(layers=24, gpt=(12288, 96), kraken4=(7424, 58), kraken8=(5472, 57)),
+}
+ENGINE_VOCAB = 51200
+ENGINE_POSITIONS = 2048
+
+
+def engine_workload(model: str, arch: str, ctx: int, layers: Optional[int] = None,
+                    dtype: str = "f16") -> "Workload":
+    """The engine of ``model`` for architecture ``arch`` ("gpt", "parallel", "kraken4" or
+    "kraken8"), one prompt of ``ctx`` tokens, random weights, fp16 (Section 4.3)."""
+    e = ENGINES[model]
+    L = layers or e["layers"]
+    if arch in ("gpt", "parallel"):
+        d, H = e["gpt"]
+        return Workload(f"{arch}-{model}-l{L}-s{ctx}", 1, L, d, H, 4 * d, dtype,
+                        seq_lens=(ctx,), arch=arch, head_size=e.get("gpt_head", 0),
+                        vocab=ENGINE_VOCAB, max_positions=ENGINE_POSITIONS)
+    n = {"kraken4": 4, "kraken8": 8}[arch]
+    d, H = e[arch]
+    return Workload(f"kraken{n}-{model}-l{L}-s{ctx}", n, L, d, H, 2 * d, dtype,
+                    seq_lens=(ctx,), vocab=ENGINE_VOCAB, max_positions=ENGINE_POSITIONS)
+
+
 _TENSOR_IDS = {"hidden": 1, "ln1_g": 2, "ln1_b": 3, "Wqkv": 4, "bqkv": 5, "Wo": 6, "bo": 7,
                "ln2_g": 8, "ln2_b": 9, "W1": 10, "b1": 11, "W2": 12, "b2": 13,
-               "W_concat": 14, "lens": 15, "cache_k": 16, "cache_v": 17}
+               "W_concat": 14, "lens": 15, "cache_k": 16, "cache_v": 17, "tokens": 18,
+               "tok_emb": 19, "pos_emb": 20, "lnf_g": 21, "lnf_b": 22}
 
 
 def workload(name: str) -> Workload:
@@ -148,8 +190,11 @@ def gen_hidden(w: Workload, n_tokens: int, seed: int = 0, device="cpu") -> torch
 
 def gen_sub_layer(w: Workload, layer: int, sub: int, seed: int = 0, device="cpu",
                   affine: str = "plain") -> Dict[str, torch.Tensor]:
-    """Parameters of sub-layer ``sub`` of layer ``layer`` (x @ W layout, [in, out])."""
+    """Parameters of sub-layer ``sub`` of layer ``layer`` (x @ W layout, [in, out]); the
+    attention width is n_heads * head_dim (d unless a head size is given).  A parallel
+    attention + FFN layer has no second LayerNorm."""
     d, f, dkv = w.d_model, w.d_ff, w.kv_width
+    dq = w.n_heads * w.head_dim
     dt = torch_dtype(w)
     ostd = w.out_proj_std if w.out_proj_std is not None else w.w_std
 
@@ -166,14 +211,18 @@ def gen_sub_layer(w: Workload, layer: int, sub: int, seed: int = 0, device="cpu"
 
     if affine not in ("plain", "random"):
         raise ValueError(f"unknown affine variant {affine!r}")
-    return {
+    p = {
         "ln1_g": vec("ln1_g", d, "gamma"), "ln1_b": vec("ln1_b", d, "beta"),
-        "Wqkv": mat("Wqkv", (d, d + 2 * dkv), w.w_std), "bqkv": vec("bqkv", d + 2 * dkv, "bias"),
-        "Wo": mat("Wo", (d, d), ostd), "bo": vec("bo", d, "bias"),
+        "Wqkv": mat("Wqkv", (d, dq + 2 * dkv), w.w_std),
+        "bqkv": vec("bqkv", dq + 2 * dkv, "bias"),
+        "Wo": mat("Wo", (dq, d), ostd), "bo": vec("bo", d, "bias"),
         "ln2_g": vec("ln2_g", d, "gamma"), "ln2_b": vec("ln2_b", d, "beta"),
         "W1": mat("W1", (d, f), w.w_std), "b1": vec("b1", f, "bias"),
         "W2": mat("W2", (f, d), ostd), "b2": vec("b2", d, "bias"),
     }
+    if w.arch == "parallel":
+        del p["ln2_g"], p["ln2_b"]
+    return p
 
 
 def gen_layer(w: Workload, layer: int, seed: int = 0, device="cpu",
@@ -185,6 +234,30 @@ def gen_w_concat(w: Workload, seed: int = 0, device="cpu") -> torch.Tensor:
     """``W_concat`` ``[N*d, d]`` ~ N(0, 0.02)."""
     return _normal((w.n_sub * w.d_model, w.d_model), _key(seed, _TENSOR_IDS["W_concat"]),
                    w.w_std, 0.0, device, torch_dtype(w))
+
+
+def gen_tokens(w: Workload, n_tokens: int, seed: int = 0) -> np.ndarray:
+    """Token ids ~ U{0 .. vocab - 1} (int32, host): a prompt of random tokens."""
+    rng = np.random.default_rng([seed, _TENSOR_IDS["tokens"]])
+    return rng.integers(0, w.vocab, size=n_tokens).astype(np.int32)
+
+
+def gen_embeddings(w: Workload, seed: int = 0, device="cpu",
+                   affine: str = "plain") -> Dict[str, torch.Tensor]:
+    """Token embedding ``[vocab, d]`` and position embedding ``[max_positions, d]`` ~
+    N(0, 0.02), the final LayerNorm (gamma = 1, beta = 0, or the random affine variant)."""
+    d, dt = w.d_model, torch_dtype(w)
+    out = {"tok_emb": _normal((w.vocab, d), _key(seed, _TENSOR_IDS["tok_emb"]), w.w_std, 0.0,
+                              device, dt),
+           "pos_emb": _normal((w.max_positions, d), _key(seed, _TENSOR_IDS["pos_emb"]), w.w_std,
+                              0.0, device, dt)}
+    if affine == "plain":
+        out["lnf_g"] = torch.ones(d, dtype=dt, device=device)
+        out["lnf_b"] = torch.zeros(d, dtype=dt, device=device)
+    else:
+        out["lnf_g"] = _normal((d,), _key(seed, _TENSOR_IDS["lnf_g"]), 0.1, 1.0, device, dt)
+        out["lnf_b"] = _normal((d,), _key(seed, _TENSOR_IDS["lnf_b"]), 0.02, 0.0, device, dt)
+    return out
 
 
 def compute_dtype(w: Workload) -> torch.dtype:

@@ -44,9 +44,12 @@ def test_blob_elems_matches_oracle_parameter_count():
 
 def _create_status(**kw):
     base = dict(n_sub=2, n_layers=2, d_model=128, n_heads=4, d_ff=0, max_tokens=64, dtype="bf16")
+    arch = kw.pop("arch", None)
     base.update(kw)
     cfg = K().Config(**base)
     c = cfg.c_struct()
+    if arch is not None:
+        c.arch = arch
     h = ctypes.c_void_p()
     st = K().lib().kraken_create(ctypes.byref(c), ctypes.byref(h))
     assert not h.value
@@ -56,10 +59,13 @@ def _create_status(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(n_sub=0), 1), (dict(n_layers=0), 1), (dict(d_model=0), 1), (dict(n_heads=0), 1),
     (dict(max_tokens=0), 1), (dict(d_ff=-1), 1), (dict(d_model=130, n_heads=4), 1),
-    (dict(d_model=128, n_heads=8), 2),        # head size 16
-    (dict(d_model=96, n_heads=3), 2),         # d not a multiple of 64
+    (dict(d_model=120, n_heads=10), 2),       # head size 12: not a multiple of 8
+    (dict(d_model=130, n_heads=2, head_dim=64), 2),   # d not a multiple of 4
     (dict(d_model=1280, n_heads=4), 2),       # head size 320
-    (dict(d_ff=100), 2), (dict(max_tokens=1 << 23), 2),
+    (dict(head_dim=136), 2),                  # head size above 128
+    (dict(d_ff=102), 2), (dict(max_tokens=1 << 23), 2),
+    (dict(arch=5), 1), (dict(n_sub=2, arch=1), 1), (dict(n_sub=2, arch=2), 1),
+    (dict(vocab=100, max_positions=0), 1), (dict(vocab=-1), 1),
     (dict(d_model=2048, n_heads=16, d_ff=8192, max_tokens=65536), 2),   # 32-bit GEMM offsets
 ])
 def test_create_rejects_bad_configs_before_allocating(kw, status):
@@ -239,3 +245,44 @@ def test_noalloc_scratch_size_matches_the_header():
     text = open(HEADER).read()
     m = re.search(r"#define KRAKEN_NOALLOC_SCRATCH_FLOATS \((\d+) \* (\d+) \* (\d+)\)", text)
     assert m and int(m[1]) * int(m[2]) * int(m[3]) == K().NOALLOC_SCRATCH_FLOATS
+
+
+def test_blob_elems_of_the_three_architectures_and_the_embeddings():
+    # GPT-like and parallel: one record per layer, no W_concat; parallel without ln2;
+    # head size other than d / heads; embeddings after the layers
+    d, F, H, hd, L, V, P = 320, 1280, 2, 128, 3, 1000, 64
+    for arch in ("gpt", "parallel", "kraken"):
+        N = 3 if arch == "kraken" else 1
+        cfg = K().Config(n_sub=N, n_layers=L, d_model=d, n_heads=H, d_ff=F, max_tokens=16,
+                         arch=arch, head_dim=hd, vocab=V, max_positions=P)
+        dq = H * hd
+        per = d * 3 * dq + 3 * dq + dq * d + d + 2 * d * F + F + d + 2 * d
+        per += 2 * d if arch != "parallel" else 0
+        want = L * N * per + (N * d * d if arch == "kraken" else 0) + (V + P) * d + 2 * d
+        assert K().weight_blob_elems(cfg) == want, arch
+    # the engine table's parameter counts (Section 4.3) with F = 2d and no biases: the
+    # blob minus biases and LayerNorms is N * 8 d^2 per layer
+    for N, d, H in [(4, 1248, 12), (8, 960, 10), (4, 3120, 30), (8, 2304, 32)]:
+        cfg = K().Config(n_sub=N, n_layers=1, d_model=d, n_heads=H, d_ff=2 * d, max_tokens=16)
+        extra = N * (4 * d + 3 * d + d + 2 * d + d) + N * d * d   # biases, LNs, W_concat
+        assert K().weight_blob_elems(cfg) - extra == N * 8 * d * d
+
+
+def test_forward_tokens_rejects_bad_arguments_before_the_device():
+    L = K().lib()
+    ids = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    cu = (ctypes.c_int32 * 2)(0, 4)
+    assert L.kraken_forward_tokens(None, ids, cu, 1, None, None, None) == K().ERR_INVALID_ARG
+
+
+def test_class_flops_of_the_comparison_architectures():
+    cu = [0, 128]
+    for arch, N in (("gpt", 1), ("parallel", 1), ("kraken", 4)):
+        cfg = K().Config(n_sub=N, n_layers=2, d_model=320, n_heads=2, d_ff=1280, head_dim=128,
+                         max_tokens=128, arch=arch, vocab=1000, max_positions=128)
+        dq = 256
+        assert K().class_flops(cfg, K().K_GEMM_QK, cu) == 2 * N * 2.0 * 128 * 320 * 2 * dq
+        assert K().class_flops(cfg, K().K_GEMM_O, cu) == 2 * N * 2.0 * 128 * dq * 320
+        assert K().class_flops(cfg, K().K_ATTN, cu) == 2 * N * 4.0 * dq * 128 * 129 / 2
+        assert K().class_flops(cfg, K().K_UNEMBED, cu) == 2.0 * 1 * 320 * 1000
+        assert (K().class_flops(cfg, K().K_CONCAT, cu) > 0) == (arch == "kraken")
