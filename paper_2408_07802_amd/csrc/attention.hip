@@ -105,6 +105,40 @@ __device__ __forceinline__ void dma16_off(uint32_t lds_addr, const void* base, u
                   "s"(reinterpret_cast<const void*>(bu)) : "memory", "m0");
 }
 
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource for raw (unstructured) access to the part from byte `off` on of the
+// `bytes` bytes at `base` (nothing when off >= bytes): no stride, no swizzle, 32-bit data
+// format.  A buffer access whose byte offset lies beyond the part reads zero and never
+// faults.  All of it is scalar arithmetic.
+__device__ __forceinline__ i32x4 raw_rsrc(const void* base, uint32_t bytes, uint32_t off) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base) + off;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu);
+  r[2] = __builtin_amdgcn_readfirstlane(off < bytes ? bytes - off : 0u);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// dma16 through a buffer resource: lane i's 16 bytes at byte offset `off` (range checked)
+// land at LDS address lds_addr + 16 i; ordered like dma16.
+__device__ __forceinline__ void dma16_buf(uint32_t lds_addr, i32x4 rsrc, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(off), "s"(rsrc)
+               : "memory", "m0");
+}
+
+// A pointer that is the same for every lane, moved to scalar registers (each half taken
+// as unsigned before widening, like dma16_off's base).
+template <typename T>
+__device__ __forceinline__ const T* uniform_ptr(const T* ptr) {
+  const uint64_t v = reinterpret_cast<uint64_t>(ptr);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+  return reinterpret_cast<const T*>(((uint64_t)hi << 32) | (uint64_t)lo);
+}
+
 // Key row read by fragment row r: bits 2 and 3 of r swapped.
 __device__ __forceinline__ int kperm(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -177,9 +211,12 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
 
   __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
 
-  // ---- which (sub-layer, head, sequence, query tile)
+  // ---- which (sub-layer, head, sequence, query tile): the same for every lane (kept in
+  // scalar registers, see attn_pp_kernel)
   int x, rank;
   head_rank_of(blockIdx.x, p.n * p.n_heads, p.tile_prefix[p.num_seqs], p.head_group, x, rank);
+  x = __builtin_amdgcn_readfirstlane(x);
+  rank = __builtin_amdgcn_readfirstlane(rank);
   const int i = x / p.n_heads;
   const int h = x - i * p.n_heads;
   int lo = 0, hi = p.num_seqs - 1;           // last b with tile_prefix[b] <= rank
@@ -187,7 +224,7 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
     const int mid = (lo + hi + 1) >> 1;
     if (p.tile_prefix[mid] <= rank) lo = mid; else hi = mid - 1;
   }
-  const int b = lo;
+  const int b = __builtin_amdgcn_readfirstlane(lo);
   const int ntiles_b = p.tile_prefix[b + 1] - p.tile_prefix[b];
   const int qt = ntiles_b - 1 - (rank - p.tile_prefix[b]);
   const int seq_start = p.cu[b], seq_end = p.cu[b + 1];
@@ -195,15 +232,17 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
   const int q_hi = min(q0 + BQ, seq_end);
   const int kv_begin = seq_start & ~7;       // 16-byte aligned V^T chunks
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int wq0 = q0 + wave * QW;
 
   const int64_t ld_qk = (int64_t)p.d + p.dkv;
   const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
   const int hkv = h / p.group;              // the key/value head this head reads
-  const S* Kbase = qkz + p.d + hkv * HD;
-  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv;
+  const S* Kbase = uniform_ptr(qkz + p.d + hkv * HD);
+  const S* Vbase =
+      uniform_ptr(static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv);
 
   // ---- Q fragments (B operand of S^T = K Q^T): lane's query, chunk 2*kc + lhalf
   uint4 qf[NQB][NQC];
@@ -433,10 +472,13 @@ __global__ __launch_bounds__(BQ / NQB / 32 * 64, 1) void attn_kernel(AttnParams 
 // through a 4-stage LDS ring.  Numbering the intervals between barriers (interval k ends
 // at barrier k), the leading group runs M(t) in interval 2t+1 and V(t) in 2t+2, the
 // trailing group one interval later; so K(u) is read in intervals 2u+1 and 2u+2, V(u) in
-// 2u+3 and 2u+4.  Every wave issues its share of tile u in interval 2u-3 (leading group
-// in M(u-2), trailing group in V(u-3)), when tile u-4, the stage's previous tile, is no
-// longer read, and waits for that share just before barrier 2u (leading group in V(u-1),
-// trailing group in M(u-1)), so the tile is complete before its first reader.
+// 2u+3 and 2u+4.  Every wave issues its share of tile u right after its M(u-2) (interval
+// 2u-3 for the leading group, 2u-2 for the trailing one), when tile u-4, the stage's
+// previous tile, is no longer read (its last reader ends in interval 2u-4), and waits for
+// that share just before barrier 2u (leading group in V(u-1), trailing group in M(u-1)),
+// so the tile is complete before its first reader.  The K/V^T loads are buffer loads
+// straight into LDS whose range check zero-fills rows past the key range: no branch and
+// no per-lane clamping; tiles past the end are loaded too (they read nothing).
 constexpr int PP_STAGES = 4;
 
 template <int N>
@@ -505,8 +547,14 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
 
   __shared__ __attribute__((aligned(16))) uint4 smem[PP_STAGES * STAGE / 16];
 
+  // The workgroup's (sub-layer, head, sequence, query tile) is the same for every lane.
+  // readfirstlane tells the compiler so (it cannot see it through the search loop): the
+  // per-tile DMA addresses and branches then run on the scalar unit instead of as 64-bit
+  // vector multiplies and exec-mask branches that compete with the other wave's softmax.
   int x, rank;
   head_rank_of(blockIdx.x, p.n * p.n_heads, p.tile_prefix[p.num_seqs], p.head_group, x, rank);
+  x = __builtin_amdgcn_readfirstlane(x);
+  rank = __builtin_amdgcn_readfirstlane(rank);
   const int i = x / p.n_heads;
   const int h = x - i * p.n_heads;
   int lo = 0, hi = p.num_seqs - 1;
@@ -514,7 +562,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     const int mid = (lo + hi + 1) >> 1;
     if (p.tile_prefix[mid] <= rank) lo = mid; else hi = mid - 1;
   }
-  const int b = lo;
+  const int b = __builtin_amdgcn_readfirstlane(lo);
   const int ntiles_b = p.tile_prefix[b + 1] - p.tile_prefix[b];
   const int qt = ntiles_b - 1 - (rank - p.tile_prefix[b]);
   const int seq_start = p.cu[b], seq_end = p.cu[b + 1];
@@ -537,8 +585,9 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   const int64_t ld_qk = (int64_t)p.d + p.dkv;
   const S* qkz = static_cast<const S*>(p.qk) + (int64_t)i * p.T * ld_qk;
   const int hkv = h / p.group;              // the key/value head this head reads
-  const S* Kbase = qkz + p.d + hkv * HD;
-  const S* Vbase = static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv;
+  const S* Kbase = uniform_ptr(qkz + p.d + hkv * HD);
+  const S* Vbase =
+      uniform_ptr(static_cast<const S*>(p.vt) + ((int64_t)i * p.dkv + hkv * HD) * p.ldv);
 
   uint4 qf[NQC];
   {
@@ -550,12 +599,17 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   }
   __builtin_amdgcn_s_waitcnt(VMCNT0);        // (visible to the compiler: see attn_kernel)
 
-  // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES.
-  // Lane offsets within a tile are computed once; a tile that ends inside the key range
-  // then costs one uniform base pointer (scalar arithmetic) per operand.  Only a tile
-  // reaching past the end of the key range clamps each lane's row.
+  // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES, as
+  // buffer loads.  Lane offsets within a tile are computed once; a tile moves the buffer
+  // resource (scalar arithmetic), whose range check replaces any clamping: K rows from T
+  // on (the sequence's last tile, and the tiles past the end that the pipeline loads
+  // without a branch) and V^T bytes past the head's rows read as zeros, and no key they
+  // hold is ever unmasked.  Any 32-bit tile offset is safe: out of range reads nothing.
+  // (The host sends only key ranges whose byte offsets fit in 32 bits here.)
   const uint32_t smem_base =
       __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)smem);
+  const uint32_t kbytes = (uint32_t)(((int64_t)p.T * ld_qk - p.d - hkv * HD) * 2);
+  const uint32_t vbytes = (uint32_t)((int64_t)HD * p.ldv * 2);
   uint32_t koff[KI], voff[VI];
 #pragma unroll
   for (int k = 0; k < KI; ++k) {
@@ -570,41 +624,20 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     voff[k] = (uint32_t)((row * (int64_t)p.ldv + lch * EPC) * 2);
   }
   auto issue = [&](int u) {
-    if (u >= n_tiles) return;
     const int kt0 = kv_begin + u * BKV;
     const uint32_t st = smem_base + (uint32_t)((u % PP_STAGES) * STAGE);
-    unsigned char* base = reinterpret_cast<unsigned char*>(smem) + (u % PP_STAGES) * STAGE;
-    if (kt0 + BKV <= p.T) {
-      const S* kb = Kbase + (int64_t)kt0 * ld_qk;
+    const i32x4 kr = raw_rsrc(Kbase, kbytes, (uint32_t)((int64_t)kt0 * ld_qk * 2));
+    const i32x4 vr = raw_rsrc(Vbase, vbytes, (uint32_t)(kt0 * 2));
 #pragma unroll
-      for (int k = 0; k < KI; ++k) dma16_off(st + (uint32_t)((wave * KI + k) * 1024), kb, koff[k]);
-    } else {
+    for (int k = 0; k < KI; ++k) dma16_buf(st + (uint32_t)((wave * KI + k) * 1024), kr, koff[k]);
 #pragma unroll
-      for (int k = 0; k < KI; ++k) {
-        const int ins = wave * KI + k;
-        const int row = ins * (64 / CHK) + lane / CHK;
-        const int lch = (lane % CHK) ^ row_key<CHK>(row);
-        const int key = min(kt0 + row, p.T - 1);
-        dma16(Kbase + (int64_t)key * ld_qk + lch * EPC, base + ins * 1024);
-      }
-    }
-    if (kt0 + BKV <= p.ldv) {
-      const S* vb = Vbase + kt0;
-#pragma unroll
-      for (int k = 0; k < VI; ++k)
-        dma16_off(st + (uint32_t)(TILE + (wave * VI + k) * 1024), vb, voff[k]);
-    } else {
-#pragma unroll
-      for (int k = 0; k < VI; ++k) {
-        const int ins = wave * VI + k;
-        const int row = ins * (64 / VCH) + lane / VCH;
-        const int lch = (lane % VCH) ^ row_key<VCH>(row);
-        const int key = min(kt0 + lch * EPC, p.ldv - EPC);
-        dma16(Vbase + (int64_t)row * p.ldv + key, base + TILE + ins * 1024);
-      }
-    }
+    for (int k = 0; k < VI; ++k)
+      dma16_buf(st + (uint32_t)(TILE + (wave * VI + k) * 1024), vr, voff[k]);
   };
-  // this wave's share of tile u is complete (u + 1 may still be in flight)
+  // Every wave issues each tile, real or past the end, so before the barrier that makes
+  // tile u readable only tile u + 1 may still be in flight; the last tile's wait drains
+  // everything.  (The branch matters to the compiler: with a loop body of one basic block
+  // its register allocation spills.)
   auto wait_tile = [&](int u) {
     if (u + 1 < n_tiles) wait_vm<NPT>();
     else wait_vm<0>();
@@ -767,44 +800,34 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     l_run += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
   };
 
-  // ---- prologue: group A loads tiles 0, 1, group B tiles 0, 1, 2 (their later loads are
-  // issued in M(t) and V(t)); tile 0 complete at barrier 0
+  // ---- prologue.  The ring starts at zero: LDS holds whatever the previous workgroup
+  // left, a range-checked load need not write the bytes of its out-of-range lanes, and a
+  // zero weight times a stale NaN would not be zero.  Then every wave loads its share of
+  // tiles 0 and 1 (later tiles are issued after M(t)); tile 0 complete at barrier 0.
+  for (int k = tid; k < PP_STAGES * STAGE / 16; k += NW * 64) smem[k] = make_uint4(0, 0, 0, 0);
+  __syncthreads();
   issue(0);
   issue(1);
-  if (trail) {
-    issue(2);
-    if (n_tiles > 2) wait_vm<2 * NPT>();
-    else if (n_tiles > 1) wait_vm<NPT>();
-    else wait_vm<0>();
-  } else {
-    if (n_tiles > 1) wait_vm<NPT>();
-    else wait_vm<0>();
-  }
+  wait_tile(0);
   __syncthreads();
   if (trail) __syncthreads();                 // group B: one interval behind
 
   for (int t = 0; t < n_tiles; ++t) {
-    // ---- M(t)
+    // ---- M(t), then this wave's share of tile t + 2
     if (t <= wlast + 1) mphase(t);
-    if (!trail) {
-      issue(t + 2);
-    } else {
-      wait_tile(t + 1);
-    }
+    issue(t + 2);
+    if (trail) wait_tile(t + 1);
     __syncthreads();
     // ---- V(t)
     if (t <= wlast) vphase(t);
-    if (!trail) {
-      wait_tile(t + 1);
-    } else {
-      issue(t + 3);
-    }
+    if (!trail) wait_tile(t + 1);
     __syncthreads();
   }
   // ---- M(n): the last PV
   if (n_tiles <= wlast + 1) mphase(n_tiles);
   __syncthreads();
   if (!trail) __syncthreads();                // group A: matches group B's extra barrier
+  wait_vm<0>();                               // no DMA into this LDS after the workgroup
 
   // ---- normalise and write O (lane: query, features ob*32 + (r/4)*8 + 4*lhalf + r%4)
   {
@@ -836,14 +859,18 @@ constexpr int nqb_for() {
 template <typename S, int HD>
 void launch_hd(const AttnParams& p, dim3 grid, hipStream_t s) {
   constexpr int NQB = nqb_for<S, HD>();
-  // (the ping-pong form needs enough MFMA work per tile to cover the softmax: head size 128)
+  // (the ping-pong form needs enough MFMA work per tile to cover the softmax: head size 128;
+  // its buffer loads address one layer's Q|K rows with 32-bit byte offsets)
   if constexpr (sizeof(S) == 2 && HD == 128) {
-    if (p.q_prescaled)
-      hipLaunchKernelGGL((attn_pp_kernel<S, HD, true>), grid, dim3(512), 0, s, p);
-    else
-      hipLaunchKernelGGL((attn_pp_kernel<S, HD, false>), grid, dim3(512), 0, s, p);
-  } else
-    hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
+    if ((int64_t)p.T * (p.d + p.dkv) * (int64_t)sizeof(S) < (int64_t)UINT32_MAX) {
+      if (p.q_prescaled)
+        hipLaunchKernelGGL((attn_pp_kernel<S, HD, true>), grid, dim3(512), 0, s, p);
+      else
+        hipLaunchKernelGGL((attn_pp_kernel<S, HD, false>), grid, dim3(512), 0, s, p);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((attn_kernel<S, HD, NQB>), grid, dim3(BQ / NQB / 32 * 64), 0, s, p);
 }
 
 template <typename S>
