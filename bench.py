@@ -47,16 +47,16 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "d3eb1be59afbc4e1b99ade4c4629882fce94a7254e174cf7e32b2e63070b87b5",
-        "read_bytes": 3240122337, "write_bytes": 269491452,
+        "source_sha256": "7c09f2846196e6546c09ccd60601338cf93050f427671be49ca229bfab407125",
+        "read_bytes": 3334295404, "write_bytes": 269220835,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
     # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
-        "source_sha256": "effd3922bb55abfeb0bc953e33b833e831c0877044923b0628aa0ef7f5d8cd97",
-        "read_bytes": 3571242872, "write_bytes": 1073882874,
+        "source_sha256": "12caf9cd5a836faacf6ba1450dfa4d3db174b870eca8c97091242b4a7dd51807",
+        "read_bytes": 3304906821, "write_bytes": 1073873269,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
