@@ -125,9 +125,10 @@ typedef enum {
  *              weight tying)
  *   max_positions  position embedding rows (>= 1 when vocab > 0): the longest
  *              sequence kraken_forward_tokens accepts
- *   Weights: d_ff * d * 4, (query + key/value widths) * d * 4, n_sub * d^2 * 4
- *   (Kraken) and vocab * d * 4 (stored widths) must stay below 2^31 (32-bit byte
- *   offsets of the repacked weights).
+ *   Weights: d_ff * d * es, (query + key/value widths) * d * es, n_sub * d^2 * es
+ *   (Kraken) and vocab * d * es (stored widths; es = 4 bytes for fp32 MFMA operands,
+ *   2 for 16-bit ones) must stay below 2^31 (32-bit byte offsets of the repacked
+ *   weights); d (stored) at most 16384.
  */
 typedef struct {
   int32_t n_sub;

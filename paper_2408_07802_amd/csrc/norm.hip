@@ -17,7 +17,7 @@ namespace kraken {
 namespace {
 
 constexpr int NORM_THREADS = 256;
-constexpr int MAX_VEC = 8;   // float4 per thread -> d <= 8192
+constexpr int MAX_VEC = 16;  // float4 per thread -> d <= 16384
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -117,11 +117,11 @@ __device__ __forceinline__ void row_stats(const float4* v, int nv, int dl, float
   rstd = rsqrtf(var + eps);
 }
 
-// Float4s per thread a row of d floats needs at most (1, 2, 4 or MAX_VEC): the kernels'
+// Float4s per thread a row of d floats needs at most (1, 2, 4, 8 or MAX_VEC): the kernels'
 // register arrays are sized by it, so a short row keeps occupancy high.
 inline int vecs_for(int d) {
   const int v = (d / 4 + NORM_THREADS - 1) / NORM_THREADS;
-  return v <= 1 ? 1 : v <= 2 ? 2 : v <= 4 ? 4 : MAX_VEC;
+  return v <= 1 ? 1 : v <= 2 ? 2 : v <= 4 ? 4 : v <= 8 ? 8 : MAX_VEC;
 }
 
 // Number of float4s this thread owns in a row of d floats.
@@ -375,6 +375,7 @@ hipError_t launch_layernorm(DType dt, const float* x, int64_t xs, const float* g
       case 1: hipLaunchKernelGGL((layernorm_kernel<S, 1>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       case 2: hipLaunchKernelGGL((layernorm_kernel<S, 2>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       case 4: hipLaunchKernelGGL((layernorm_kernel<S, 4>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 8: hipLaunchKernelGGL((layernorm_kernel<S, 8>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       default: hipLaunchKernelGGL((layernorm_kernel<S, MAX_VEC>), grid, block, 0, s, x, xs, gamma, beta, o, n, T, d, dl, eps, ovf); break;
     }
     return hipGetLastError();
@@ -395,6 +396,7 @@ hipError_t launch_combine_ln2(DType dt, const float* x, const float* shared, con
       case 1: hipLaunchKernelGGL((combine_ln2_kernel<S, 1>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       case 2: hipLaunchKernelGGL((combine_ln2_kernel<S, 2>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       case 4: hipLaunchKernelGGL((combine_ln2_kernel<S, 4>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
+      case 8: hipLaunchKernelGGL((combine_ln2_kernel<S, 8>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
       default: hipLaunchKernelGGL((combine_ln2_kernel<S, MAX_VEC>), grid, block, 0, s, x, shared, h, gamma, beta, o, n, T, d, dl, eps, ovf); break;
     }
     return hipGetLastError();

@@ -255,28 +255,31 @@ kraken_status validate_cfg(const kraken_config* c) {
   if (D.dq % 64 != 0)
     return fail(KRAKEN_ERR_UNSUPPORTED,
                 "n_heads * stored head size (32, 64 or 128) must be a multiple of 64");
-  if (D.dp > 8192) return fail(KRAKEN_ERR_UNSUPPORTED, "d_model above 8192");
+  if (D.dp > 16384) return fail(KRAKEN_ERR_UNSUPPORTED, "d_model above 16384");
   if (c->max_tokens > (1 << 22)) return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens above 4194304");
   if (c->vocab > 0 && c->max_positions < 1)
     return fail(KRAKEN_ERR_INVALID_ARG, "a model with embeddings needs max_positions >= 1");
-  // GEMM operands of one sub-layer are addressed with 32-bit byte offsets: the activation
-  // rows (tokens x the widest stored row), and the repacked weights [out][in] of the
-  // projections, the FFN (Fp x dp either way), W_concat (dp x N dp) and the token
-  // embedding (V x dp); 4 bytes bounds every element type
-  const int64_t widest = std::max<int64_t>({(int64_t)D.dp, D.dq + D.dkv, (int64_t)D.Fp});
-  if ((int64_t)c->max_tokens * widest * 4 >= (1ll << 31))
-    return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens * the widest activation row too large");
-  if ((int64_t)D.Fp * D.dp * 4 >= (1ll << 31) || (D.dq + D.dkv) * D.dp * 4 >= (1ll << 31))
-    return fail(KRAKEN_ERR_UNSUPPORTED, "d_ff * d_model too large for 32-bit weight offsets");
-  if (c->arch == KRAKEN_ARCH_KRAKEN && (int64_t)D.N * D.dp * D.dp * 4 >= (1ll << 31))
-    return fail(KRAKEN_ERR_UNSUPPORTED,
-                "n_sub * d_model^2 too large for 32-bit W_concat offsets");
-  if ((int64_t)D.V * D.dp * 4 >= (1ll << 31))
-    return fail(KRAKEN_ERR_UNSUPPORTED, "vocab * d_model too large for 32-bit offsets");
   if (c->dtype < KRAKEN_DTYPE_F32 || c->dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
   if (c->compute < KRAKEN_COMPUTE_STORAGE || c->compute > KRAKEN_COMPUTE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown compute type");
+  // GEMM operands of one sub-layer are addressed with 32-bit byte offsets: the activation
+  // rows (tokens x the widest stored row; 4 bytes bounds every activation type), and the
+  // repacked weights [out][in] in the compute type (es bytes) of the projections, the FFN
+  // (Fp x dp either way), W_concat (dp x N dp) and the token embedding (V x dp)
+  const bool f32_ops = c->compute == KRAKEN_COMPUTE_F32 ||
+                       (c->compute == KRAKEN_COMPUTE_STORAGE && c->dtype == KRAKEN_DTYPE_F32);
+  const int64_t es = f32_ops ? 4 : 2;
+  const int64_t widest = std::max<int64_t>({(int64_t)D.dp, D.dq + D.dkv, (int64_t)D.Fp});
+  if ((int64_t)c->max_tokens * widest * 4 >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "max_tokens * the widest activation row too large");
+  if ((int64_t)D.Fp * D.dp * es >= (1ll << 31) || (D.dq + D.dkv) * D.dp * es >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "d_ff * d_model too large for 32-bit weight offsets");
+  if (c->arch == KRAKEN_ARCH_KRAKEN && (int64_t)D.N * D.dp * D.dp * es >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED,
+                "n_sub * d_model^2 too large for 32-bit W_concat offsets");
+  if ((int64_t)D.V * D.dp * es >= (1ll << 31))
+    return fail(KRAKEN_ERR_UNSUPPORTED, "vocab * d_model too large for 32-bit offsets");
   return KRAKEN_OK;
 }
 
@@ -1196,7 +1199,7 @@ kraken_status kraken_op_layernorm(int32_t dtype, const float* x, int64_t xs, con
   if (!x || !gamma || !beta || !out) return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
   if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
-  if (n < 1 || T < 0 || d < 4 || d % 64 != 0 || d > 8192 || xs < 0)
+  if (n < 1 || T < 0 || d < 4 || d % 64 != 0 || d > 16384 || xs < 0)
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
   hipError_t e = launch_layernorm((DType)dtype, x, xs, gamma, beta, out, n, T, d, d, eps, nullptr,
                                   static_cast<hipStream_t>(stream));
@@ -1211,7 +1214,7 @@ kraken_status kraken_op_combine_ln2(int32_t dtype, const float* x, const float* 
     return fail(KRAKEN_ERR_INVALID_ARG, "NULL pointer");
   if (dtype < KRAKEN_DTYPE_F32 || dtype > KRAKEN_DTYPE_F16)
     return fail(KRAKEN_ERR_UNSUPPORTED, "unknown dtype");
-  if (n < 1 || T < 0 || d % 64 != 0 || d < 64 || d > 8192)
+  if (n < 1 || T < 0 || d % 64 != 0 || d < 64 || d > 16384)
     return fail(KRAKEN_ERR_INVALID_ARG, "bad sizes");
   hipError_t e = launch_combine_ln2((DType)dtype, x, shared, h, gamma, beta, out, n, T, d, d, eps,
                                     nullptr, static_cast<hipStream_t>(stream));

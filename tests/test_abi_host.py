@@ -67,6 +67,7 @@ def _create_status(**kw):
     (dict(arch=5), 1), (dict(n_sub=2, arch=1), 1), (dict(n_sub=2, arch=2), 1),
     (dict(vocab=100, max_positions=0), 1), (dict(vocab=-1), 1),
     (dict(d_model=2048, n_heads=16, d_ff=8192, max_tokens=65536), 2),   # 32-bit GEMM offsets
+    (dict(d_model=16448, n_heads=128, head_dim=128, d_ff=64, max_tokens=1), 2),  # width
 ])
 def test_create_rejects_bad_configs_before_allocating(kw, status):
     assert _create_status(**kw) == status
@@ -159,10 +160,12 @@ def test_create_rejects_bad_kv_heads(kw, status):
 
 
 @pytest.mark.parametrize("kw", [
-    # repacked FFN weights F x d past 2^31 bytes at 4 bytes an element
-    dict(d_model=8192, n_heads=64, d_ff=65536, max_tokens=1),
-    # W_concat^T d x N d past 2^31 bytes
-    dict(n_sub=16, d_model=8192, n_heads=64, d_ff=8192, max_tokens=1),
+    # repacked FFN weights F x d past 2^31 bytes: fp32 operands (4 bytes an element), and
+    # 16-bit operands (2 bytes)
+    dict(d_model=8192, n_heads=64, d_ff=65536, max_tokens=1, dtype="f32"),
+    dict(d_model=8192, n_heads=64, d_ff=131072, max_tokens=1),
+    # W_concat^T d x N d past 2^31 bytes at 2 bytes an element
+    dict(n_sub=32, d_model=8192, n_heads=64, d_ff=8192, max_tokens=1),
 ])
 def test_create_rejects_weight_offsets_past_32_bits(kw):
     assert _create_status(**kw) == K().ERR_UNSUPPORTED

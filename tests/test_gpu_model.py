@@ -254,3 +254,13 @@ def test_engine_shapes_128_token_prompt(model, arch):
     last token's logits and every hidden row against the oracle."""
     w = synth.engine_workload(model, arch, 128)
     logits_vs_oracle(w, [128], affine="plain")
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("arch", ["gpt", "kraken8"])
+def test_175b_engine_widths_two_layers(arch):
+    """The 175B engines' widths at two layers: the GPT-like d = 12288 (LayerNorm rows of 12
+    float4 per thread, FFN 49152 wide) and the 8-way Kraken d = 5472 (57 heads of 96,
+    padded to 5504 and 128), fp16, one 64-token prompt."""
+    w = synth.engine_workload("175b", arch, 64, layers=2)
+    logits_vs_oracle(w, [64], affine="plain")

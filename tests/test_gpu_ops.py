@@ -49,7 +49,8 @@ def check_close(got, ref, dtype_name, what, rel_elem=None, rel_rms=None):
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("n,T,d,shared", [(3, 37, 128, False), (2, 5, 2048, True),
                                           (4, 130, 768, False), (1, 1, 64, False),
-                                          (2, 9, 8192, False), (8, 3, 2048, True)])
+                                          (2, 9, 8192, False), (8, 3, 2048, True),
+                                          (2, 3, 12288, False), (1, 2, 16384, True)])
 def test_layernorm(dtype, n, T, d, shared):
     g = torch.Generator(device="cpu").manual_seed(n * 1000 + T * 7 + d)
     x = (torch.randn((1 if shared else n, T, d), generator=g) * 3 + 1.5).to(DEV)
@@ -69,7 +70,8 @@ def test_layernorm(dtype, n, T, d, shared):
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("n,T,d,shared", [(2, 64, 128, True), (2, 64, 128, False),
                                           (4, 33, 768, False), (8, 17, 2048, False),
-                                          (1, 5, 1280, False), (3, 2, 4096, True)])
+                                          (1, 5, 1280, False), (3, 2, 4096, True),
+                                          (2, 3, 12288, False), (1, 2, 16384, True)])
 def test_combine_ln2(dtype, n, T, d, shared):
     g = torch.Generator(device="cpu").manual_seed(n * 31 + T + d)
     x = torch.randn((n, T, d), generator=g).to(DEV)
