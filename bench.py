@@ -15,6 +15,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                                         (one decode step of B sequences of C cached
                                           tokens each: decode tokens/s and an HBM
                                           roofline of its dominant kernel)
+       python bench.py --graph          (the timed steps replay the prefill captured
+                                          once as a HIP graph)
        python bench.py --share G        (one GPU's part of a G-way split: N/G
                                           sub-layers per layer, no exchange)
        python bench.py --engine MODEL --arch ARCH --ctx C
@@ -360,6 +362,8 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048, help="with --engine: prompt length")
     ap.add_argument("--layers", type=int, default=0, help="with --engine: layer count "
                                                           "(0: the engine's)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the prefill as one captured HIP graph (replayed per step)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
@@ -423,6 +427,21 @@ def main():
     for _ in range(args.warmup):
         model.prefill(X, cu, out=out)
     torch.cuda.synchronize()
+    step = lambda: model.prefill(X, cu, out=out)
+    if args.graph:
+        # the whole prefill recorded once as a HIP graph (on a side stream, as capture
+        # requires) and replayed per step on the current stream: the same kernels and
+        # arguments, without the host's per-launch cost
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(graph, stream=side):
+            model.prefill(X, cu, out=out)
+        torch.cuda.synchronize()
+        step = graph.replay
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
 
     # ---- timed region: K steps, no instrumentation (an event between steps: the per-step
     # TTFT distribution; events on the prefill's stream cost nothing measurable)
@@ -433,7 +452,7 @@ def main():
     wall0 = time.perf_counter()
     ev0.record(stream)
     for k in range(args.steps):
-        model.prefill(X, cu, out=out)
+        step()
         evs[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -494,7 +513,8 @@ def main():
         "config": {"workload": w.name, "n_sub": w.n_sub, "n_layers": w.n_layers,
                    "d_model": w.d_model, "n_heads": w.n_heads, "n_kv_heads": w.kv_heads,
                    "d_ff": w.d_ff, "seq_lens": lens, "tokens": T, "storage_dtype": w.dtype,
-                   "mfma_operands": compute, "accumulate": "f32"},
+                   "mfma_operands": compute, "accumulate": "f32",
+                   "launch": "hip_graph" if args.graph else "stream"},
         "mfma_util_pct": 100.0 * total_flops / (ms_per_step * 1e-3) / (peak * 1e12),
         "phase_mfma_util_pct": {
             "gemm": 100.0 * gemm_fl / (gemm_ms * 1e-3) / (peak * 1e12),

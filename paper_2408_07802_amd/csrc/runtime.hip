@@ -704,7 +704,11 @@ kraken_status check_cache(const kraken_model* m, const void* cache, int32_t max_
 extern "C" {
 
 const char* kraken_status_string(kraken_status s) {
-  switch (s) {
+  // A C caller may pass any int; in C++ an enum object holding a value outside the enum's
+  // range is undefined behaviour, so the code is read as the int it is.
+  int code;
+  std::memcpy(&code, &s, sizeof code);
+  switch (code) {
     case KRAKEN_OK: return "ok";
     case KRAKEN_ERR_INVALID_ARG: return "invalid argument";
     case KRAKEN_ERR_UNSUPPORTED: return "unsupported configuration";
