@@ -76,8 +76,9 @@ def rel_err(got, ref):
     return float(np.max(np.abs(np.asarray(got) - ref)) / np.sqrt(np.mean(ref ** 2)))
 
 
-def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
+def run_and_compare(w, lens, seed=0, affine="plain", prefix=None, tol=None):
     """Full-length GPU prefill; oracle on all tokens, or on the first `prefix` of each seq."""
+    tol = tol or TOL[w.dtype]
     cu = synth.cu_seqlens(lens)
     T = cu[-1]
     say(f"[prefill parity] {w.name} compute={w.compute} lens={lens[:8]} T={T} affine={affine} "
@@ -103,9 +104,9 @@ def run_and_compare(w, lens, seed=0, affine="plain", prefix=None):
                                     n_kv_heads=w.kv_heads)
     e_out = rel_err(f64(out)[rows], out_o)
     e_sub = rel_err(f64(sub)[:, rows], sub_o)
-    say(f"    max|err|/rms: out {e_out:.3e}  sub_out {e_sub:.3e}  (bound {TOL[w.dtype]})")
-    assert e_out <= TOL[w.dtype], e_out
-    assert e_sub <= TOL[w.dtype], e_sub
+    say(f"    max|err|/rms: out {e_out:.3e}  sub_out {e_sub:.3e}  (bound {tol})")
+    assert e_out <= tol, e_out
+    assert e_sub <= tol, e_sub
     return e_out, e_sub
 
 
@@ -352,6 +353,24 @@ def test_bf16_operands_n4_l12_d768_prefix():
     # bf16 MFMA operands (no fp16 conversion): within the bound at this depth
     w = dataclasses.replace(synth.workload("kraken-n4-l12-d768-h12-s2048-bf16"), compute="bf16")
     run_and_compare(w, synth.seq_lens(w), prefix=256)
+
+
+# bf16 MFMA operands at depth.  Rounding the six operand points of every sub-layer (LN1
+# out, Q|K and V, P, attention out, LN2 out, GELU out) to bf16 (unit roundoff 2^-9) grows
+# the error with depth: a float64 emulation of exactly that rounding gives about 2.1e-2
+# at 36 layers, past the 2e-2 bound of the fp16-operand path, so these runs are held to
+# twice the emulated error of the deepest workload.
+BF16_OPERAND_TOL = 4e-2
+BF16_DEPTH_CASES = [("kraken-n4-l24-d1024-h16-s4096-bf16", 256),
+                    ("kraken-n8-l24-d2048-h16-s8192-bf16", 256),
+                    ("kraken-n4-l36-d1280-h20-ragged8x512-4096-bf16", 64)]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,prefix", BF16_DEPTH_CASES, ids=[c[0] for c in BF16_DEPTH_CASES])
+def test_bf16_operands_at_depth(name, prefix):
+    w = dataclasses.replace(synth.workload(name), compute="bf16")
+    run_and_compare(w, synth.seq_lens(w), prefix=prefix, tol=BF16_OPERAND_TOL)
 
 
 def test_fp16_operand_overflow_is_rejected_at_load():
