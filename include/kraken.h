@@ -420,6 +420,10 @@ kraken_status kraken_debug_poison_workspace(kraken_model* m, void* stream);
  *      of Q K^T directly: out = softmax(ln(2) Q K^T + mask) V.  This is the
  *      variant the prefill launches.
  *   cu_seqlens is a HOST int32[num_seqs+1] array as in kraken_prefill.
+ *   16-bit operands with hd = 128 run the ping-pong kernel the prefill uses as long
+ *   as one layer's qk rows fit 32-bit byte offsets (T * (d + dkv) * 2 < 2^32);
+ *   larger inputs, and every other case, run the one-phase kernel.  Same results
+ *   either way, within each kernel's rounding.
  */
 kraken_status kraken_op_attention(int32_t dtype, const void* qk, const void* vt, void* out,
                                   int32_t n, int32_t d, int32_t n_heads, int32_t n_kv_heads,

@@ -469,6 +469,49 @@ def test_attention_dma_base_with_bit31_of_the_low_address_word_set_and_clear():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.timeout(600)
+def test_attention_past_32_bit_qk_offsets_takes_the_one_phase_kernel():
+    """One layer's Q|K rows of more than 4 GiB (T (d + dkv) 2 bytes > 2^32, here 65,537
+    tokens of d = dkv = 16,384, 128 heads of 128): the ping-pong kernel addresses them with
+    32-bit byte offsets, so the launch takes the one-phase kernel.  Sampled query rows of
+    two heads against the oracle's single-row attention (a row attends to itself and the
+    keys before it), under the elementwise bound of the kernel's rounding model."""
+    n, d, H, hd = 1, 16384, 128, 128
+    T = (1 << 32) // (2 * d * 2) + 1
+    assert T * 2 * d * 2 > (1 << 32) - 1
+    dt = torch.float16
+    c = LOG2E / math.sqrt(hd)
+    g = torch.Generator(device=DEV).manual_seed(1729)
+    qk = torch.empty((n, T, 2 * d), dtype=dt, device=DEV)
+    qk[:, :, :d] = (torch.randn((n, T, d), generator=g, device=DEV) * (1.5 * c)).to(dt)
+    qk[:, :, d:] = (torch.randn((n, T, d), generator=g, device=DEV) * 1.5).to(dt)
+    v = torch.randn((n, T, d), generator=g, device=DEV).to(dt)
+    vt = torch.zeros((n, d, K().vt_ld(T)), dtype=dt, device=DEV)
+    vt[:, :, :T] = v.transpose(1, 2)
+    out = torch.full((n, T, d), float("nan"), dtype=dt, device=DEV)
+    print(f"[attention 32-bit fallback] T={T} d={d} H={H}", flush=True)
+    K().op_attention(qk, vt, out, n, d, H, [0, T], q_prescaled=True)
+    torch.cuda.synchronize()
+    rows = [0, 1, 63, 64, 4095, 30001, T - 2, T - 1]
+    for h in (0, 77):
+        cols = slice(h * hd, (h + 1) * hd)
+        q64 = f64(qk[0, :, cols]) / c
+        k64 = f64(qk[0, :, d + h * hd:d + (h + 1) * hd])
+        v64 = f64(v[0, :, cols])
+        got = f64(out[0, rows, cols])
+        for j, r in enumerate(rows):
+            args = (q64[r:r + 1], k64[r:r + 1])
+            ref = O.cached_attention(*args, v64[r:r + 1], [k64[:r]], [v64[:r]], 1)[0]
+            wabs = O.cached_attention(*args, np.abs(v64[r:r + 1]), [k64[:r]],
+                                      [np.abs(v64[:r])], 1)[0]
+            bound = 2.0 ** -11 * (wabs + np.abs(ref)) + 1e-6 * np.sqrt(np.mean(ref ** 2))
+            err = np.abs(got[j] - ref)
+            assert np.all(np.isfinite(got[j])), (h, r)
+            assert np.all(err <= bound), (h, r, float(np.max(err / bound)))
+    del qk, vt, v, out
+    torch.cuda.empty_cache()
+
+
 # ----------------------------------------------------------------------- decode attention
 
 DECODE_ATTN_CASES = [
