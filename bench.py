@@ -49,8 +49,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "7c09f2846196e6546c09ccd60601338cf93050f427671be49ca229bfab407125",
-        "read_bytes": 3334295404, "write_bytes": 269220835,
+        "source_sha256": "9c867122863beb9459cae10a910194052a28bb159635aeed1b7c5dd2c203d363",
+        "read_bytes": 3293564904, "write_bytes": 269268955,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },

@@ -602,10 +602,11 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   // this wave's share of the DMA of key tile u (K and V^T) into stage u % PP_STAGES, as
   // buffer loads.  Lane offsets within a tile are computed once; a tile moves the buffer
   // resource (scalar arithmetic), whose range check replaces any clamping: K rows from T
-  // on (the sequence's last tile, and the tiles past the end that the pipeline loads
-  // without a branch) and V^T bytes past the head's rows read as zeros, and no key they
-  // hold is ever unmasked.  Any 32-bit tile offset is safe: out of range reads nothing.
-  // (The host sends only key ranges whose byte offsets fit in 32 bits here.)
+  // on (the sequence's last tile) and V^T bytes past the head's rows read as zeros, and no
+  // key they hold is ever unmasked.  The tiles past the end that the pipeline loads
+  // without a branch get an empty range and read nothing.  Any 32-bit tile offset is
+  // safe: out of range reads nothing.  (The host sends only key ranges whose byte offsets
+  // fit in 32 bits here.)
   const uint32_t smem_base =
       __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_ptr)smem);
   const uint32_t kbytes = (uint32_t)(((int64_t)p.T * ld_qk - p.d - hkv * HD) * 2);
@@ -627,7 +628,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     const int kt0 = kv_begin + u * BKV;
     const uint32_t st = smem_base + (uint32_t)((u % PP_STAGES) * STAGE);
     const i32x4 kr = raw_rsrc(Kbase, kbytes, (uint32_t)((int64_t)kt0 * ld_qk * 2));
-    const i32x4 vr = raw_rsrc(Vbase, vbytes, (uint32_t)(kt0 * 2));
+    const i32x4 vr = raw_rsrc(Vbase, u < n_tiles ? vbytes : 0u, (uint32_t)(kt0 * 2));
 #pragma unroll
     for (int k = 0; k < KI; ++k) dma16_buf(st + (uint32_t)((wave * KI + k) * 1024), kr, koff[k]);
 #pragma unroll
