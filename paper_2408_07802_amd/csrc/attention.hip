@@ -694,6 +694,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) pb[sb][hh] = make_uint4(0, 0, 0, 0);
   const f32x16 zero16 = {};
+  uint4 vpre[RING];                           // first V^T fragments of the next M phase
 
   // M(t): PV(t-1) and S(t), alternating.  At t = 0 P is zero and V is read from tile 0's
   // stage (real data), so the PV MFMAs add exactly zero; for t > wlast the scores are never
@@ -707,12 +708,18 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
     uint4 kf[RING], vf[RING];
     sfor<0, RING>([&](auto J) {
       kf[J()] = k_frag(kst, J());
-      vf[J()] = v_frag(vst, J());
+      vf[J()] = vpre[J()];
     });
+    // slot order PV0, PV1, S0, PV2, S1, ..., PV15, S14, S15: the V^T fragments of the
+    // first PV MFMAs are already in registers, and the K fragment reads issued at the
+    // start of the phase land under them
     sfor<0, 2 * NS>([&](auto Sl) {
       constexpr int sl = decltype(Sl)::value;
-      constexpr int j = sl >> 1;
-      if constexpr ((sl & 1) == 0) {
+      constexpr bool pv = sl < 2 || (sl < 2 * NS - 2 && (sl & 1));
+      constexpr int j = sl < 2 ? sl
+                        : pv ? (sl - 3) / 2 + 2
+                        : sl < 2 * NS - 2 ? (sl - 2) / 2 : sl - NS;
+      if constexpr (pv) {
         constexpr int sb = j / (2 * OB), hh = (j / OB) & 1, ob = j % OB;
         oacc[ob] = mfma_chunk<S>(vf[j % RING], pb[sb][hh], oacc[ob]);
         if constexpr (j + RING < NP) vf[j % RING] = v_frag(vst, j + RING);
@@ -728,6 +735,9 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
 
   // V(t): online softmax of S(t) into P(t)
   auto vphase = [&](int t) {
+    // the next matrix phase's first V^T fragments (tile t: complete since M(t)), read
+    // here so that their latency passes under the softmax
+    sfor<0, RING>([&](auto J) { vpre[J()] = v_frag(stage_off(t), J()); });
     const int kt0 = kv_begin + t * BKV;
     // keys outside [seq_start, my_q] get weight 0 (only tiles crossing the diagonal or the
     // sequence start): register r of key block sb holds key kt0 + 8 lhalf + off(r)
@@ -811,6 +821,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
   issue(1);
   wait_tile(0);
   __syncthreads();
+  sfor<0, RING>([&](auto J) { vpre[J()] = v_frag(stage_off(0), J()); });
   if (trail) __syncthreads();                 // group B: one interval behind
 
   for (int t = 0; t < n_tiles; ++t) {
