@@ -49,16 +49,16 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "9c867122863beb9459cae10a910194052a28bb159635aeed1b7c5dd2c203d363",
-        "read_bytes": 3293564904, "write_bytes": 269268955,
+        "source_sha256": "c83fd59895606ac222dd2b65cdb4acde8b16ee7358f7dd218770b047cd467ce6",
+        "read_bytes": 3279526916, "write_bytes": 269143075,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
     # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
-        "source_sha256": "12caf9cd5a836faacf6ba1450dfa4d3db174b870eca8c97091242b4a7dd51807",
-        "read_bytes": 3304906821, "write_bytes": 1073873269,
+        "source_sha256": "2435912463645ede7213596ce41cbe543ff9a5c4f3321d78f4c90b6ac4cfd80b",
+        "read_bytes": 3222943404, "write_bytes": 1073814371,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
