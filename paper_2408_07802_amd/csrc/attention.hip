@@ -753,60 +753,76 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnParams p) {
           sacc[sb][r] = (off - lo_ <= span) ? sacc[sb][r] : -INFINITY;
         }
     }
-    // (four independent chains of three-input maxima, not one chain of 16)
-    float mq[4];
+    // Weights, packed to 16 bits for the PV MFMAs; the row sums add the packed (rounded)
+    // weights, i.e. exactly the ones the MFMAs multiply (four independent partial sums).
+    // The scores stay in sacc, so that the exact path below can start over from them.
+    float lsum[4];
+    auto weights = [&]() {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f32x16& sq = sacc[q >> 1];
-      const int o = 8 * (q & 1);
-      mq[q] = fmaxf(sq[o], sq[o + 1]);
+      for (int sb = 0; sb < 2; ++sb) {
+        typedef S s8 __attribute__((ext_vector_type(8)));
 #pragma unroll
-      for (int r = 2; r < 8; r += 2) mq[q] = fmaxf(fmaxf(mq[q], sq[o + r]), sq[o + r + 1]);
-    }
-    const float mraw = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-    float mx = fmaxf(m_run, PRE ? mraw + c0 : mraw * scale);
-    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
-                                                     false, false);
-    mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    // the exponent base moves only when a maximum outgrows it by more than 8 (log2):
-    // weights stay <= 2^8 and rescales of O are rare
-    if (__ballot(mx > m_run + 8.0f)) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
-      l_run *= alpha;
+        for (int hh = 0; hh < 2; ++hh) {
+          s8 v;
 #pragma unroll
-      for (int ob = 0; ob < OB; ++ob)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[ob][r] *= alpha;
-      if constexpr (PRE) {
-        const float shift = mx - c0;
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[sb][r] -= shift;
-        c0 = mx;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) cneg[r] = -mx;
+          for (int k = 0; k < 8; ++k) {
+            const float x = sacc[sb][8 * hh + k];
+            v[k] = (S)(PRE ? __builtin_amdgcn_exp2f(x)
+                           : __builtin_amdgcn_exp2f(fmaf(x, scale, -m_run)));
+          }
+          pb[sb][hh] = __builtin_bit_cast(uint4, v);
+          lsum[2 * sb + hh] = sum8<S>(pb[sb][hh], 0.f);
+        }
       }
-      m_run = mx;
+    };
+    // The exponent base moves only when a maximum outgrows it by more than 8 (log2):
+    // weights stay <= 2^8 and rescales of O are rare.  After the first tile the weights
+    // are taken against the current base straight away, and the row maximum is computed
+    // only if some lane's packed row sum reaches 2^8: a weight above 2^8 rounds to at
+    // least 2^8 in 16 bits and no sum of non-negative weights is smaller than any of
+    // them, so every tile that needs a new base takes the exact path, which decides as
+    // if there were no shortcut (the results are the same bit for bit).
+    bool exact = t == 0;
+    if (!exact) {
+      weights();
+      exact = __ballot((lsum[0] + lsum[1]) + (lsum[2] + lsum[3]) >= 256.0f) != 0;
     }
-    // weights, packed to 16 bits for the PV MFMAs; the row sum adds the packed (rounded)
-    // weights, i.e. exactly the ones the MFMAs multiply (four independent partial sums)
-    float lsum[4] = {0.f, 0.f, 0.f, 0.f};
+    if (exact) {
+      // (four independent chains of three-input maxima, not one chain of 16)
+      float mq[4];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& sq = sacc[q >> 1];
+        const int o = 8 * (q & 1);
+        mq[q] = fmaxf(sq[o], sq[o + 1]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sacc[sb][r] = PRE ? __builtin_amdgcn_exp2f(sacc[sb][r])
-                          : __builtin_amdgcn_exp2f(fmaf(sacc[sb][r], scale, -m_run));
-      typedef S s8 __attribute__((ext_vector_type(8)));
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        s8 v;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = (S)sacc[sb][8 * hh + k];
-        pb[sb][hh] = __builtin_bit_cast(uint4, v);
-        lsum[2 * sb + hh] = sum8<S>(pb[sb][hh], lsum[2 * sb + hh]);
+        for (int r = 2; r < 8; r += 2) mq[q] = fmaxf(fmaxf(mq[q], sq[o + r]), sq[o + r + 1]);
       }
+      const float mraw = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+      float mx = fmaxf(m_run, PRE ? mraw + c0 : mraw * scale);
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      if (__ballot(mx > m_run + 8.0f)) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
+        l_run *= alpha;
+#pragma unroll
+        for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[ob][r] *= alpha;
+        if constexpr (PRE) {
+          const float shift = mx - c0;
+#pragma unroll
+          for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sacc[sb][r] -= shift;
+          c0 = mx;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) cneg[r] = -mx;
+        }
+        m_run = mx;
+      }
+      weights();
     }
     l_run += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
   };
