@@ -49,8 +49,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "c83fd59895606ac222dd2b65cdb4acde8b16ee7358f7dd218770b047cd467ce6",
-        "read_bytes": 3279526916, "write_bytes": 269143075,
+        "source_sha256": "d0409147ec269c5a346cfc9ce100b9ab840b91e12db2f38ad1695c9e681c4d5a",
+        "read_bytes": 3260107817, "write_bytes": 269233804,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
