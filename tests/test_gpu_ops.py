@@ -415,6 +415,42 @@ def test_attention_prescaled_q(dtype, case):
                     f"pre-scaled attention sub-layer {i}")
 
 
+@pytest.mark.parametrize("pre", [True, False])
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_attention_rising_scores_take_every_softmax_path(dtype, pre):
+    """Ping-pong attention (head size 128, Q pre-scaled or not) on scores that climb by ~2.5
+    (log2 units) per 64-key tile over the first 1100 keys and then drop by 10.  The
+    running maximum outgrows the exponent base every few tiles (rescales of O); most
+    tiles in between have packed row sums of 2^8 or more while staying within 8 of the
+    base (the exact path, which then keeps the base); the low tail takes the shortcut
+    without a maximum.  Every query sees the same profile up to its own position."""
+    n, d, H, T = 1, 256, 2, 1700
+    hd = d // H
+    cu = [0, T]
+    dt = tdt(dtype)
+    g = torch.Generator(device="cpu").manual_seed(77)
+    q = torch.randn((n, T, d), generator=g) * 0.1           # Q in log2-unit scale
+    k = torch.randn((n, T, d), generator=g) * 0.1
+    v = torch.randn((n, T, d), generator=g).to(dt)
+    t = torch.arange(T, dtype=torch.float32)
+    score = torch.where(t < 1100, 2.5 * t / 64, torch.full_like(t, 2.5 * 1100 / 64 - 10))
+    score = score + 0.5 * torch.sin(t)
+    for h in range(H):
+        q[:, :, h * hd] = 1.0
+        k[:, :, h * hd] = score
+    c = LOG2E / math.sqrt(hd)
+    qk = torch.cat([(q if pre else q / c).to(dt), k.to(dt)], dim=2)
+    vt = torch.zeros((n, d, K().vt_ld(T)), dtype=dt)
+    vt[:, :, :T] = v.transpose(1, 2)
+    print(f"[attention rising scores] T={T} {dtype} q_prescaled={pre}", flush=True)
+    out = torch.full((n, T, d), float("nan"), dtype=dt, device=DEV)
+    K().op_attention(qk.to(DEV), vt.to(DEV), out, n, d, H, cu, q_prescaled=pre)
+    torch.cuda.synchronize()
+    q64 = qk[0, :, :d].double().numpy() / (c if pre else 1.0)
+    check_heads(f64(out[0]), q64, qk[0, :, d:].double().numpy(), v[0].double().numpy(), cu,
+                H, None, dtype, "attention with rising scores")
+
+
 def test_attention_dma_base_with_bit31_of_the_low_address_word_set_and_clear():
     """Regression test of a fixed fault.  The ping-pong attention kernel rebuilds each
     wave-uniform 64-bit DMA base from two 32-bit halves; the low half must be widened as
