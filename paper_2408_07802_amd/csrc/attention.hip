@@ -15,7 +15,8 @@
 // once per tile with the partner lane (lane ^ 32).  The output is accumulated
 // transposed, O^T = V^T P^T, whose columns are again the lane's query, so the
 // rescale by exp(m_old - m_new) is lane-local; the exponent base only moves when
-// a maximum outgrows it by more than 2^8, so rescales are rare.  P^T goes from the
+// a maximum exceeds it by more than 8 in base-2 log units (a weight would pass 2^8),
+// so rescales are rare.  P^T goes from the
 // S^T accumulator registers straight into the B operand of the second MFMA.  The K
 // rows of each 32-row fragment are read in an order that swaps bits 2 and 3 of the
 // row index; then result
@@ -28,6 +29,8 @@
 // other's MFMAs do) or, for tiles that do not split over 8 waves, 4 waves of 64.
 // K and V^T tiles of 64 keys are copied from HBM straight into a 3-stage LDS
 // ring (global_load_lds_dwordx4), two tiles ahead of the tile being computed.
+// 16-bit operands with head size 128 take the ping-pong form further down (a 4-stage
+// ring of range-checked buffer loads, the two waves of a SIMD in opposite phases).
 // Workgroups are ordered heaviest (longest causal prefix) first.
 #include <type_traits>
 
