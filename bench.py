@@ -49,8 +49,8 @@ COPY_PROBE_BYTES = 1 << 30
 TRAFFIC = {
     "attention": {
         "source": "paper_2408_07802_amd/csrc/attention.hip",
-        "source_sha256": "d0409147ec269c5a346cfc9ce100b9ab840b91e12db2f38ad1695c9e681c4d5a",
-        "read_bytes": 3260107817, "write_bytes": 269233804,
+        "source_sha256": "d36a3271213cc855a692f8cbe52ca89e197b506421157266e20b90d46b78bc18",
+        "read_bytes": 3262133080, "write_bytes": 269231327,
         "algorithmic_bytes": 4 * 8 * 8192 * 2048 * 2,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
