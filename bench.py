@@ -57,8 +57,8 @@ TRAFFIC = {
     # FFN up projection with the GELU epilogue (A: LN2 output, B: W1, C: the activation)
     "gemm_up": {
         "source": "paper_2408_07802_amd/csrc/gemm.hip",
-        "source_sha256": "2435912463645ede7213596ce41cbe543ff9a5c4f3321d78f4c90b6ac4cfd80b",
-        "read_bytes": 3222943404, "write_bytes": 1073814371,
+        "source_sha256": "e3b5be6adeb3c4bc7aa9a2404ce5950c6ec763f2b666b5b3039215acb20837bb",
+        "read_bytes": 3224425359, "write_bytes": 1074040672,
         "algorithmic_bytes": 2 * (8 * 8192 * 2048 * 2 + 8 * 8192 * 8192) + 8 * 8192 * 4,
         "profile": "profiles/hbm_traffic_n8_l24_d2048_t8192.md",
     },
